@@ -1,0 +1,50 @@
+"""The denoise loop with classifier-free guidance and DDIM, resumable at step k.
+
+Test infrastructure only (see the package docstring).
+
+Approximate caching (Sec. 2.1; worker behaviour in Sec. 4.5 and Sec. 4.7) takes
+the intermediate latent of a cached prompt at iteration K and runs the
+remaining N-K iterations conditioned on the new prompt. Here that is
+``denoise(..., start_step=K, n_steps=N-K)``: the latent passed in is x at
+``timesteps[K]``, and iteration i (K <= i < K+n) maps x at ``timesteps[i]`` to
+x at ``timesteps[i+1]`` (the sentinel -1 stands for the clean sample).
+"""
+
+import numpy as np
+
+from . import schedule as S
+from .unet import forward
+
+
+def abar_table(cfg):
+    return S.alphas_cumprod(S.betas(cfg.n_train_steps, cfg.beta_start, cfg.beta_end, cfg.beta_schedule))
+
+
+def step(cfg, W, x, ctx, t, t_prev, cfg_scale, abar=None):
+    """One guided DDIM iteration for a batch of B latents.
+
+    x [B, c, H, W] fp32; ctx [2B, L, D] = B unconditional then B conditional rows.
+    The UNet runs once on [x; x] (effective batch 2B). Returns
+    (eps_raw [2B, c, H, W], eps_guided [B, c, H, W], x_next [B, c, H, W])."""
+    if abar is None:
+        abar = abar_table(cfg)
+    b = x.shape[0]
+    eps_raw = forward(cfg, W, np.concatenate([x, x], axis=0), t, ctx)
+    eps = S.cfg(eps_raw[:b], eps_raw[b:], cfg_scale)
+    x_next = S.ddim_step(x, eps, S.abar_at(abar, t), S.abar_at(abar, t_prev))
+    return eps_raw, eps, x_next.astype(np.float32)
+
+
+def denoise(cfg, W, x, ctx, timesteps, start_step, n_steps, cfg_scale, trace=None):
+    """Run iterations start_step .. start_step + n_steps - 1; returns the final latent.
+    If ``trace`` is a list, the latent after every iteration is appended to it."""
+    ts = np.asarray(timesteps)
+    if start_step < 0 or n_steps < 0 or start_step + n_steps + 1 > ts.size:
+        raise ValueError("timesteps too short for start_step + n_steps")
+    abar = abar_table(cfg)
+    x = np.asarray(x, dtype=np.float32).copy()
+    for i in range(start_step, start_step + n_steps):
+        _, _, x = step(cfg, W, x, ctx, int(ts[i]), int(ts[i + 1]), cfg_scale, abar)
+        if trace is not None:
+            trace.append(x.copy())
+    return x
