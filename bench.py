@@ -1,0 +1,290 @@
+"""Benchmark: denoise steps/s and images/s at SD-XL shapes (50 DDIM steps with
+classifier-free guidance, batch 1 -> UNet batch 2), on one MI355X.
+
+A benchmark step is one image: dn_denoise over all 50 iterations from a fresh
+latent (every row of the hot path: time embedding, conv_in, ResNet blocks,
+transformers, down/up sampling, out head, guidance + DDIM). Inputs (random
+weights ~ N(0, 1/fan_in), latent and context ~ N(0, 1)) are generated on the
+device before timing. Prints one JSON line.
+
+Extra fields: the dominant kernel's roofline (the FF-in GEGLU GEMM of the
+32x32 transformer blocks, timed live with HIP events on the library's stream),
+the approximate-caching k-sweep (lookup over 100,000 cached embeddings + resume
+at step k), and the CPU oracle timed on a bounded sample on the host.
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def unet_flops(cfg, n):
+    """(conv + linear, attention) FLOPs of one UNet evaluation on n samples (2 per MAC)."""
+    c0, temb = cfg.model_channels, 4 * cfg.model_channels
+    H, W = cfg.latent_h, cfg.latent_w
+    lin = 2 * n * (c0 * temb + temb * temb) + 2 * n * H * W * c0 * cfg.latent_c * 9
+    att = 0.0
+    skips = [c0]
+    ch = c0
+
+    def res(cin, cout, hw):
+        f = 2 * n * hw * cout * 9 * (cin + cout) + 2 * n * temb * cout
+        return f + (2 * n * hw * cout * cin if cin != cout else 0)
+
+    def tx(c, depth, hw):
+        tok = n * hw
+        per = 2 * tok * c * c * 6 + 4 * n * cfg.ctx_len * cfg.ctx_dim * c + 2 * tok * c * c * 3 * cfg.ff_mult
+        return 4 * tok * c * c + depth * per, depth * (4 * n * hw * hw * c + 4 * n * hw * cfg.ctx_len * c)
+
+    L = len(cfg.levels)
+    for l, (c, d, _, _) in enumerate(cfg.levels):
+        for _ in range(cfg.layers_per_block):
+            lin += res(ch, c, H * W)
+            ch = c
+            if d:
+                a, b = tx(c, d, H * W)
+                lin, att = lin + a, att + b
+            skips.append(ch)
+        if l < L - 1:
+            H, W = H // 2, W // 2
+            lin += 2 * n * H * W * c * c * 9
+            skips.append(ch)
+    c = cfg.levels[-1][0]
+    lin += res(ch, c, H * W) + res(c, c, H * W)
+    if cfg.mid_depth > 0:
+        a, b = tx(c, cfg.mid_depth, H * W)
+        lin, att = lin + a, att + b
+    for l in reversed(range(L)):
+        c, d, _, _ = cfg.levels[l]
+        for _ in range(cfg.layers_per_block + 1):
+            lin += res(ch + skips.pop(), c, H * W)
+            ch = c
+            if d:
+                a, b = tx(c, d, H * W)
+                lin, att = lin + a, att + b
+        if l > 0:
+            H, W = H * 2, W * 2
+            lin += 2 * n * H * W * c * c * 9
+    lin += 2 * n * H * W * cfg.latent_c * ch * 9
+    return lin, att
+
+
+def device_weights(torch, dn, cfg, seed):
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    table = dn.weight_table(cfg)
+    blob = torch.empty(sum(t[0] for t in table), device="cuda")
+    off = 0
+    for numel, fan, kind in table:
+        v = blob[off:off + numel]
+        if kind in (0, 1):
+            v.normal_(0.0, fan ** -0.5, generator=g)
+        elif kind == 2:
+            v.normal_(1.0, 0.1, generator=g)
+        else:
+            v.normal_(0.0, 0.1, generator=g)
+        off += numel
+    return blob
+
+
+def roofline_ff_in(torch, dn, stream, iters=20):
+    """FF-in GEGLU GEMM of a 32x32 SD-XL transformer block: M = 2048 tokens (batch 2),
+    K = 1280, 2 x 5120 packed output columns -> 5120 GEGLU outputs."""
+    M, N, K = 2048, 5120, 1280
+    x = torch.randn((M, K), device="cuda").to(torch.bfloat16)
+    w = (torch.randn((2 * N, K), device="cuda") / math.sqrt(K)).to(torch.bfloat16)
+    b = torch.randn(2 * N, device="cuda")
+    y = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+    for _ in range(3):
+        dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True, stream=stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(iters):
+        dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True, stream=stream)
+    e1.record(stream)
+    e1.synchronize()
+    avg_s = e0.elapsed_time(e1) / 1e3 / iters
+    flops = 2.0 * M * (2 * N) * K
+    achieved = flops / avg_s / 1e12
+    return {"kernel": "gemm_kernel<bf16,256,linear> FF-in GEGLU 2048x10240x1280", "bound": "mfma",
+            "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "avg_launch_us": round(avg_s * 1e6, 2), "flops_per_launch": flops}
+
+
+def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, queries=4):
+    """Approximate caching: lookup + latent fetch + resume at k for 50 - k steps."""
+    from paper_2511_06724_amd import workloads as W
+    cache = torch.from_numpy(W.cache_embeddings(n_entries, dim, seed=7).view("uint16")).cuda()
+    qs, rows = W.planted_queries(cache.cpu().numpy().view("float16"), queries, seed=9)
+    # cached latents: 100,000 x 4 x 128 x 128 bf16 = 13.1 GB, drawn on the device
+    g = torch.Generator(device="cuda").manual_seed(8)
+    lat_cache = torch.empty((n_entries, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda",
+                            dtype=torch.bfloat16)
+    for s in range(0, n_entries, 10_000):
+        lat_cache[s:s + 10_000].normal_(generator=g)
+    qd = [torch.from_numpy(q.view("uint16").copy()).cuda() for q in qs]
+    # lookup timing (warm: the 153.6 MB table is resident in the 256 MB last-level cache after one pass)
+    dn.ac_lookup(qd[0], cache)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for q in qd:
+        idx, _ = dn.ac_lookup(q, cache)
+    t_lookup = (time.perf_counter() - t0) / len(qd)
+    ok = all(dn.ac_lookup(q, cache)[0] == int(r) for q, r in zip(qd, rows))
+    lat = torch.empty((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda")
+    out = {"lookup_us_per_query": round(t_lookup * 1e6, 1),
+           "lookup_GBps": round(n_entries * dim * 2 / t_lookup / 1e9, 1), "planted_found": ok, "k": {}}
+    for k in (0, 5, 10, 15, 20, 25):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for q in qd[:2]:
+            idx, _ = dn.ac_lookup(q, cache)
+            dn.ac_fetch_latent(lat_cache, idx, lat)
+            model.denoise(lat, ctx, ts, k, 50 - k, 7.5)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / 2
+        out["k"][str(k)] = round(1.0 / dt, 4)
+        print(f"[bench] ac k={k}: {1.0 / dt:.3f} images/s", file=sys.stderr, flush=True)
+    del lat_cache
+    return out
+
+
+def cpu_baseline(sample_blocks=4):
+    """The CPU oracle on the host cores: one SD-XL 32x32 transformer stage (C = 1280,
+    20 heads x 64, batch 2 with guidance) of `sample_blocks` blocks plus one top-level
+    ResBlock (128x128, C = 320), timed, then scaled by FLOPs to a full denoise step."""
+    import numpy as np
+    from oracle import unet as OU
+    from paper_2511_06724_amd import workloads as W
+    import oracle.topology as OT
+
+    threads = len(os.sched_getaffinity(0))
+    cfg = W.sdxl()
+    sub = cfg.with_(levels=((320, 0, 5, 64), (640, 0, 10, 64), (1280, sample_blocks, 20, 64)))
+    rng = np.random.default_rng(0)
+    names = [r for r in OT.tensor_table(sub) if r[0].startswith("down2.0.tx") or r[0].startswith("down0.0.res")]
+    Wt = {}
+    for name, shape, kind, fan in names:
+        if kind in ("w", "b"):
+            Wt[name] = (rng.standard_normal(shape, dtype=np.float32) / np.float32(math.sqrt(fan)))
+        elif kind == "g":
+            Wt[name] = 1 + 0.1 * rng.standard_normal(shape, dtype=np.float32)
+        else:
+            Wt[name] = 0.1 * rng.standard_normal(shape, dtype=np.float32)
+    x_tx = rng.standard_normal((2, 1280, 32, 32), dtype=np.float32)
+    x_res = rng.standard_normal((2, 320, 128, 128), dtype=np.float32)
+    ctx = rng.standard_normal((2, 77, 2048), dtype=np.float32)
+    temb = rng.standard_normal((2, 1280), dtype=np.float32)
+    t0 = time.perf_counter()
+    OU.transformer(sub, Wt, "down2.0.tx", x_tx, ctx, sample_blocks, 20)
+    OU.resblock(sub, Wt, "down0.0.res", x_res, temb)
+    dt = time.perf_counter() - t0
+    hw, c, tok = 1024, 1280, 2048
+    tx_flops = 4 * tok * c * c + sample_blocks * (2 * tok * c * c * 18 + 4 * 2 * 77 * 2048 * c
+                                                   + 4 * 2 * hw * hw * c + 4 * 2 * hw * 77 * c)
+    res_flops = 2 * 2 * 16384 * 320 * 9 * 640 + 2 * 2 * 1280 * 320
+    lin, att = unet_flops(cfg, 2)
+    sample_flops = tx_flops + res_flops
+    steps_per_s = (sample_flops / dt) / (lin + att)
+    return {"value": round(steps_per_s, 6), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": (f"one SD-XL 32x32 transformer stage of {sample_blocks} blocks + one 128x128 ResBlock "
+                       f"(batch 2), {sample_flops / 1e12:.3f} TFLOP in {dt:.1f} s, extrapolated by FLOPs to a "
+                       f"full {(lin + att) / 1e12:.3f} TFLOP step"),
+            "images_per_s": round(steps_per_s / 50, 8)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3, help="timed images (50 denoise iterations each)")
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ac", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the denoise loop is replicated per GPU, "
+              "with no exchange between GPUs; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2511_06724_amd import dn, workloads as W
+
+    assert torch.cuda.is_available()
+    torch.cuda.set_device(0)
+    cfg = W.sdxl(W.DN_BF16, batch=args.batch)
+    print("[bench] generating SD-XL weights on the device", file=sys.stderr, flush=True)
+    blob = device_weights(torch, dn, cfg, seed=42)
+    model = dn.Denoiser(cfg, blob)
+    del blob
+    torch.cuda.empty_cache()
+    g = torch.Generator(device="cuda").manual_seed(0)
+    x0 = torch.randn((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda", generator=g)
+    ctx = torch.randn((2 * cfg.batch, cfg.ctx_len, cfg.ctx_dim), device="cuda", generator=g)
+    from_ts = [(49 - j) * 20 + 1 for j in range(50)] + [-1]
+    import numpy as np
+    ts = np.array(from_ts, np.int32)
+    stream = torch.cuda.current_stream()
+    lat = x0.clone()
+    for i in range(args.warmup):
+        lat.copy_(x0)
+        model.denoise(lat, ctx, ts, 0, 50, 7.5, stream=stream)
+        torch.cuda.synchronize()
+        print(f"[bench] warmup image {i} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        lat.copy_(x0)
+        model.denoise(lat, ctx, ts, 0, 50, 7.5, stream=stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    finite = bool(torch.isfinite(lat).all())
+    images_per_s = args.steps * cfg.batch / dt
+    steps_per_s = args.steps * 50 / dt
+    ms_step = dt / args.steps * 1e3
+    lin, att = unet_flops(cfg, 2 * cfg.batch)
+    mfma_util = (lin + att) * steps_per_s / 1e12 / PEAK_BF16_TFLOPS
+    print(f"[bench] {steps_per_s:.2f} denoise steps/s, {images_per_s:.3f} images/s", file=sys.stderr, flush=True)
+
+    roof = roofline_ff_in(torch, dn, stream)
+    ac = None if args.no_ac else ac_sweep(torch, dn, model, cfg, ctx, ts)
+    model.close()
+    cpu = None if args.no_cpu_baseline else cpu_baseline()
+    out = {
+        "metric": "denoise steps/sec + images/sec at SD-XL shapes (50 steps, CFG); MFMA util %",
+        "value": round(steps_per_s, 3),
+        "unit": "denoise steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (random weights ~N(0,1/fan_in), latent and context ~N(0,1))",
+        "config": {"workload": "SD-XL-shaped UNet, latent 1x4x128x128, 50 DDIM steps, CFG 7.5 (UNet batch 2)",
+                   "batch": cfg.batch, "params": int(sum(t[0] for t in dn.weight_table(cfg))),
+                   "tflop_per_denoise_step": round((lin + att) / 1e12, 3)},
+        "images_per_s": round(images_per_s, 4),
+        "ms_per_denoise_step": round(dt / args.steps / 50 * 1e3, 3),
+        "mfma_util_whole_step": round(mfma_util, 4),
+        "output_finite": finite,
+        "roofline": roof,
+        "ac_sweep": ac,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,265 @@
+/*
+ * argus_dn.h — C ABI of the MI355X (gfx950) denoise-loop library.
+ *
+ * Hot path of the Argus serving method (arXiv 2511.06724): the GPU worker of
+ * Sec. 4.5 / Sec. 4.7 either starts from Gaussian noise or, under approximate
+ * caching (AC, Sec. 2.1), finds the most similar cached prompt by embedding
+ * similarity, takes that prompt's intermediate latent at iteration K and runs
+ * the remaining N-K denoising iterations conditioned on the new prompt. Each
+ * iteration is one UNet evaluation (the compute-bound component of Table 3 and
+ * Observation 5, Sec. 3.2) with classifier-free guidance, then a DDIM update.
+ *
+ * Calls:
+ *   dn_weight_count / dn_weight_table  size and describe the canonical weight blob
+ *   dn_create                          build a denoiser (pack weights for the GPU)
+ *   dn_denoise                         run iterations [start_step, start_step + n_steps)
+ *   ac_lookup                          top-1 cosine search over the prompt-embedding cache
+ *   ac_fetch_latent                    copy cached latent #idx into an fp32 latent buffer
+ *   dn_unet_eps                        one UNet evaluation + guidance (per-step check hook)
+ *   dn_op_*                            single-kernel entry points (kernel checks, timing)
+ *   dn_destroy, dn_last_error
+ *
+ * Conventions (every call):
+ *   - Pointers marked "device" are HIP device allocations owned by the caller;
+ *     they must stay valid until the work enqueued on `stream` has finished.
+ *     Pointers marked "host" are read or written during the call only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Calls that take a stream only enqueue work and return; calls that do not
+ *     take one are synchronous.
+ *   - Every argument is checked before any work is enqueued: on DN_EINVAL
+ *     nothing was enqueued and no output was touched. HIP runtime failures
+ *     return DN_EHIP. dn_last_error() gives a message for the calling thread.
+ *   - Floating-point data: fp32 = IEEE binary32; fp16 and bf16 buffers are
+ *     passed as uint16_t bit patterns (IEEE binary16 / bfloat16).
+ *   - All results are deterministic: the same inputs give bitwise equal outputs
+ *     (no floating-point atomics; all reductions run in a fixed order).
+ */
+#ifndef ARGUS_DN_H
+#define ARGUS_DN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DN_ABI_VERSION 1
+#define DN_MAX_LEVELS 4
+
+typedef struct dn_handle dn_handle; /* opaque: packed device weights + workspace */
+
+typedef enum {
+  DN_OK = 0,
+  DN_EINVAL = -1,       /* invalid argument or configuration */
+  DN_ENOMEM = -2,       /* device or host allocation failed */
+  DN_EHIP = -3,         /* HIP runtime error */
+  DN_EUNSUPPORTED = -4  /* valid but not supported by this build (e.g. no gfx950 device) */
+} dn_status;
+
+typedef enum { DN_FP32 = 0, DN_BF16 = 1 } dn_dtype;
+typedef enum { DN_WEIGHTS_HOST = 0, DN_WEIGHTS_DEVICE = 1 } dn_weights_location;
+typedef enum { DN_BETA_LINEAR = 0, DN_BETA_SCALED_LINEAR = 1 } dn_beta_schedule;
+
+/* One resolution level of the UNet. depth = transformer blocks per attention
+ * stage (0 = ResNet blocks only). heads * head_dim must equal channels. */
+typedef struct {
+  int32_t channels;
+  int32_t depth;
+  int32_t heads;
+  int32_t head_dim;
+} dn_level;
+
+/* A latent-diffusion UNet and its sampler schedule. The parameter counts of
+ * this topology reproduce Table 3's SD-XL and SD 2.0 UNets exactly (SD-XL's
+ * added-condition MLP aside, which the denoise loop does not use).
+ *
+ * dtype          DN_BF16: weights and activations bf16 with fp32 accumulation;
+ *                norm statistics, softmax, the time embedding, the transformer
+ *                residual stream, the latent and the DDIM update stay fp32.
+ *                DN_FP32: everything fp32.
+ * batch          images B; the UNet runs on 2B rows (B unconditional, then B
+ *                conditional) for classifier-free guidance.
+ * latent_*       latent channels (<= 64) and spatial size; H and W must be
+ *                divisible by 2^(n_levels-1).
+ * model_channels C0: width of conv_in and of the sinusoidal timestep features;
+ *                the time embedding has 4*C0 features.
+ * level[]        n_levels (1..4) levels, coarsening by 2 between levels.
+ * layers_per_block  ResNet(+transformer) layers per down level; up levels have one more.
+ * mid_depth      -1: no middle block; 0: ResBlock, ResBlock; >0: ResBlock,
+ *                transformer of mid_depth blocks, ResBlock (at the last level's width).
+ * tiny_topology  1: conv_in -> ResBlock -> transformer(level[0].depth) -> out head
+ *                (level 0 only; no skips, no middle block, no up path).
+ * ctx_len, ctx_dim  text-encoder context tokens and width (cross-attention keys).
+ * ff_mult        GEGLU feed-forward width multiplier (inner width ff_mult*C).
+ * gn_groups      GroupNorm groups (channel counts must be divisible by it).
+ * gn_eps         GroupNorm epsilon of ResBlocks and the out head; tx_gn_eps of
+ *                the transformer's input GroupNorm; ln_eps of its LayerNorms.
+ * n_train_steps, beta_start, beta_end, beta_schedule   the training noise
+ *                schedule; abar_t = prod_{i<=t} (1 - beta_i).
+ */
+typedef struct {
+  int32_t abi_version; /* must be DN_ABI_VERSION */
+  int32_t dtype;
+  int32_t batch;
+  int32_t latent_c, latent_h, latent_w;
+  int32_t model_channels;
+  int32_t n_levels;
+  dn_level level[DN_MAX_LEVELS];
+  int32_t layers_per_block;
+  int32_t mid_depth;
+  int32_t tiny_topology;
+  int32_t ctx_len, ctx_dim, ff_mult, gn_groups;
+  float gn_eps, tx_gn_eps, ln_eps;
+  int32_t n_train_steps;
+  float beta_start, beta_end;
+  int32_t beta_schedule;
+} dn_config;
+
+/* Number of fp32 values in the canonical weight blob of `cfg`.
+ * The blob is every tensor of the model back to back, in PyTorch layouts
+ * (conv [Cout][Cin][kh][kw], linear [out][in]), in this order:
+ *  1. time MLP: lin1.w [4C0][C0], lin1.b, lin2.w [4C0][4C0], lin2.b
+ *  2. conv_in.w [C0][latent_c][3][3], conv_in.b
+ *  3. down levels l = 0..L-1: layers_per_block x (ResBlock, then transformer if
+ *     depth_l > 0), then for l < L-1 a stride-2 downsample conv [C_l][C_l][3][3] + bias
+ *  4. middle block (mid_depth >= 0): ResBlock, transformer(mid_depth) if > 0, ResBlock
+ *  5. up levels l = L-1..0: (layers_per_block + 1) x (ResBlock on the channel
+ *     concatenation [h, skip], transformer if depth_l > 0), then for l > 0 a
+ *     nearest-x2 upsample followed by conv [C_l][C_l][3][3] + bias
+ *  6. out head: GroupNorm scale, shift [C0]; conv_out.w [latent_c][C0][3][3], conv_out.b
+ * ResBlock(Cin -> Cout): gn1 scale, shift [Cin]; conv1.w [Cout][Cin][3][3], conv1.b;
+ *   temb.w [Cout][4C0], temb.b; gn2 scale, shift [Cout]; conv2.w [Cout][Cout][3][3],
+ *   conv2.b; if Cin != Cout a 1x1 skip conv skip.w [Cout][Cin][1][1], skip.b.
+ * Transformer(C, depth): gn scale, shift; proj_in.w [C][C], proj_in.b; depth x
+ *   { ln1 scale, shift; attn1 q, k, v [C][C] (no bias); attn1 out.w [C][C], out.b;
+ *     ln2 scale, shift; attn2 q [C][C], k [C][ctx_dim], v [C][ctx_dim]; attn2 out.w, out.b;
+ *     ln3 scale, shift; ff1.w [2*F*C][C], ff1.b (first half value, second half gate);
+ *     ff2.w [C][F*C], ff2.b }; proj_out.w [C][C], proj_out.b.
+ * Returns DN_EINVAL for an invalid configuration. */
+dn_status dn_weight_count(const dn_config* cfg, size_t* n_floats);
+
+/* Describes the blob tensor by tensor: for tensor i (canonical order),
+ * numel[i] elements, fan_in[i] = the layer's input size (Cin*kh*kw or
+ * in_features; also given for its bias; 0 for norm parameters) and kind[i] =
+ * 0 weight, 1 bias, 2 norm scale, 3 norm shift. Arrays are host memory with
+ * room for `capacity` entries (NULL arrays with capacity 0 query the count);
+ * *n_tensors receives the tensor count. DN_EINVAL if capacity is too small. */
+dn_status dn_weight_table(const dn_config* cfg, int64_t* numel, int32_t* fan_in, int32_t* kind,
+                          size_t capacity, size_t* n_tensors);
+
+/* Builds a denoiser: validates cfg, copies the fp32 blob (n_floats values,
+ * host or device memory per `weights_location`) and repacks it on the GPU
+ * into kernel layouts in the configured dtype. The caller keeps ownership of
+ * the blob. Synchronous. On success *out receives the handle. */
+dn_status dn_create(const dn_config* cfg, const float* weights, size_t n_floats, int32_t weights_location,
+                    dn_handle** out);
+
+/* Denoise loop (Sec. 2.1, Sec. 4.7): for i = start_step .. start_step+n_steps-1,
+ *   eps_raw = UNet([x; x], t_i, text_ctx)             (2B rows)
+ *   eps     = eps_u + cfg_scale * (eps_c - eps_u)     (classifier-free guidance)
+ *   x       = sqrt(abar_prev) * x0 + sqrt(1 - abar_prev) * eps,
+ *             x0 = (x - sqrt(1 - abar_t) * eps) / sqrt(abar_t)   (DDIM, eta = 0)
+ * with t_i = timesteps[i], abar_t = abar[t_i], abar_prev = abar[timesteps[i+1]]
+ * and timestep -1 meaning the clean sample (abar = 1).
+ * latent     device fp32 [B][latent_c][H][W], read and updated in place: on entry
+ *            it is x at timesteps[start_step] (for AC, the cached intermediate
+ *            latent of iteration K = start_step), on return x at
+ *            timesteps[start_step + n_steps].
+ * text_ctx   device fp32 [2B][ctx_len][ctx_dim]: B unconditional rows, then B conditional.
+ * timesteps  host int32, n_timesteps >= start_step + n_steps + 1 entries, each in
+ *            [-1, n_train_steps).
+ * n_steps = 0 enqueues nothing. Asynchronous on `stream`. One handle serves one
+ * stream at a time (its workspace is reused by every call). */
+dn_status dn_denoise(dn_handle* h, float* latent, const float* text_ctx, const int32_t* timesteps,
+                     int32_t n_timesteps, int32_t start_step, int32_t n_steps, float cfg_scale, void* stream);
+
+/* One UNet evaluation + guidance at timestep t (no DDIM update), for checking a
+ * single iteration. x device fp32 [B][latent_c][H][W]; text_ctx as in dn_denoise;
+ * out_raw device fp32 [2B][latent_c][H][W] (UNet output on [x; x]);
+ * out_guided device fp32 [B][latent_c][H][W] (eps after guidance) or NULL.
+ * Asynchronous on `stream`. */
+dn_status dn_unet_eps(dn_handle* h, const float* x, int32_t t, const float* text_ctx, float cfg_scale,
+                      float* out_raw, float* out_guided, void* stream);
+
+/* Nearest cached prompt (Sec. 2.1; Sec. 4.7): argmax_i of the cosine similarity
+ * (q . c_i) / (|q| |c_i|) over the n rows of the cache, ties going to the
+ * lowest index. query_emb device fp16 [dim]; cache_embs device fp16 [n][dim]
+ * (row-major). Products and sums in fp32. On success *out_idx (host) receives
+ * the index and, if out_score (host) is not NULL, *out_score the cosine.
+ * Synchronous (default stream). n >= 1, dim >= 1; the query must be non-zero.
+ * On error *out_idx is left untouched (the caller falls back to K = 0). */
+dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64_t n, int32_t dim,
+                    int64_t* out_idx, float* out_score);
+
+/* Copies cached latent #idx of a device bf16 table [n][numel] into the device
+ * fp32 latent buffer [numel] (the resume state of Sec. 4.7). Asynchronous. */
+dn_status ac_fetch_latent(const uint16_t* cache_latents, int64_t n, int64_t numel, int64_t idx, float* latent,
+                          void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Single-kernel entry points. They run exactly the kernels dn_denoise runs and
+ * exist for element-wise checks at full size and for timing one kernel.
+ * All buffers are device memory, row-major, in the element type `dtype`
+ * (DN_BF16 -> bf16 bits, DN_FP32 -> fp32) unless stated otherwise.
+ * ------------------------------------------------------------------------- */
+
+/* Dense layer (the transformer's projections and feed-forward):
+ * y[m][n] = sum_k x[m][k] * w[n][k] + bias[n] (+ resid[m][n]).
+ * x [M][K], w [N][K], bias fp32 [N] or NULL, resid [M][N] or NULL, y [M][N].
+ * K must be a multiple of 64 (bf16) / 32 (fp32). Output fp32 when y_f32 != 0,
+ * else `dtype`; resid fp32 when resid_f32 != 0, else `dtype`.
+ * geglu != 0 (GEGLU feed-forward, Shazeer 2020): w has 2N rows and bias 2N
+ * entries, interleaved in blocks of 32 — rows [64j, 64j+32) are value rows
+ * [32j, 32j+32) and rows [64j+32, 64j+64) the matching gate rows — and
+ * y[m][n] = a * GELU(g) with a, g the value and gate outputs of column n
+ * (exact erf GELU); N % 32 == 0 and resid must be NULL. Asynchronous. */
+dn_status dn_op_linear(int32_t dtype, const void* x, const void* w, const float* bias, const void* resid,
+                       int32_t resid_f32, void* y, int32_t y_f32, int64_t M, int32_t N, int32_t K, int32_t geglu,
+                       void* stream);
+
+/* 3x3 convolution (cross-correlation, zero padding 1, bias) as an implicit GEMM
+ * on NHWC activations: x [n][H][W][Cin]; with up = 1 the input is first
+ * nearest-neighbour upsampled to 2H x 2W (never materialised); stride 1 or 2.
+ * w [Cout][3][3][Cin] (tap-major: PyTorch [Cout][Cin][3][3] permuted), bias fp32
+ * [Cout] or NULL, temb fp32 [n][Cout] or NULL (added per sample, as a ResBlock
+ * adds its time-embedding projection), resid [n][Ho][Wo][Cout] or NULL,
+ * y [n][Ho][Wo][Cout] with Ho = (Hl - 1) / stride + 1 for the logical input
+ * height Hl (same for W); fp32 output when y_f32 != 0. Cin must be a multiple
+ * of 64 (bf16) / 32 (fp32). Asynchronous. */
+dn_status dn_op_conv3x3(int32_t dtype, const void* x, int32_t n, int32_t H, int32_t W, int32_t Cin, int32_t up,
+                        int32_t stride, const void* w, const float* bias, const float* temb, const void* resid,
+                        void* y, int32_t Cout, int32_t y_f32, void* stream);
+
+/* Attention core O = softmax(Q K^T * scale) V for each (sample, head), the
+ * score matrix never materialised: q [B][Sq][ldq], k [B][Skv][ldk],
+ * v [B][Skv][ldv] (ldv == ldk), o [B][Sq][ldo]. Head h occupies columns
+ * [h * head_stride, (h + 1) * head_stride), head_stride 32 or 64; a head of
+ * d < head_stride real dimensions must hold zeros in its padding columns of
+ * q and k (the padding columns of o then receive the same mix of v's padding
+ * columns). Softmax in fp32. Asynchronous. */
+dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void* k, int32_t ldk, const void* v,
+                          int32_t ldv, void* o, int32_t ldo, int32_t B, int32_t heads, int32_t Sq, int32_t Skv,
+                          int32_t head_stride, float scale, void* stream);
+
+/* GroupNorm (Wu & He 2018) over NHWC x [n][HW][C] with G groups: biased
+ * variance, statistics from fp32 partial sums merged in fp64,
+ * y = x_hat * gamma[c] + beta[c], then SiLU if silu != 0. gamma, beta fp32 [C];
+ * C % G == 0 and C a multiple of 8. Synchronous (allocates its workspace). */
+dn_status dn_op_groupnorm(int32_t dtype, const void* x, void* y, int32_t n, int32_t HW, int32_t C, int32_t G,
+                          const float* gamma, const float* beta, float eps, int32_t silu);
+
+/* LayerNorm over the last axis: x fp32 [M][C] (the residual stream), y [M][C]
+ * in `dtype`; C a multiple of 4, at most 2048. Asynchronous. */
+dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int32_t C, const float* gamma,
+                          const float* beta, float eps, void* stream);
+
+void dn_destroy(dn_handle* h); /* NULL-safe; synchronizes the device first */
+
+const char* dn_last_error(void); /* message of the calling thread's last error, "" if none */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ARGUS_DN_H */

@@ -47,7 +47,8 @@ def conv2d(x, w, b, stride=1, pad=1):
     for i in range(kh):
         for j in range(kw):
             patch = xp[:, i:i + stride * (ho - 1) + 1:stride, j:j + stride * (wo - 1) + 1:stride, :]
-            out += (patch.reshape(-1, cin) @ w[:, :, i, j].T).reshape(n, ho, wo, cout)
+            w_tap = np.ascontiguousarray(w[:, :, i, j].T)  # [Cin, Cout]
+            out += (patch.reshape(-1, cin) @ w_tap).reshape(n, ho, wo, cout)
     out += b
     return np.ascontiguousarray(out.transpose(0, 3, 1, 2))
 

@@ -13,10 +13,15 @@ import numpy as np
 
 
 def cosine_scores(query, cache):
-    """fp64 cosine similarity of query [dim] against every row of cache [n, dim]."""
+    """fp64 cosine similarity of query [dim] against every row of cache [n, dim].
+    A zero-norm row has no defined cosine and scores -inf (it never wins)."""
     q = np.asarray(query, dtype=np.float64)
     c = np.asarray(cache, dtype=np.float64)
-    return (c @ q) / (np.linalg.norm(c, axis=1) * np.linalg.norm(q))
+    norms = np.linalg.norm(c, axis=1)
+    out = np.full(c.shape[0], -np.inf)
+    ok = norms > 0
+    out[ok] = (c[ok] @ q) / (norms[ok] * np.linalg.norm(q))
+    return out
 
 
 def top1(query, cache):

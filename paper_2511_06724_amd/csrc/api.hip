@@ -1,0 +1,320 @@
+// C ABI of the denoise-loop library: argument checks, error mapping and the
+// single-kernel entry points. Every entry point catches all C++ exceptions.
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "model.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dn_status fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return static_cast<dn_status>(code);
+}
+
+template <typename F> dn_status guarded(F&& f) {
+  try {
+    g_last_error.clear();
+    f();
+    return DN_OK;
+  } catch (const dn::Error& e) {
+    return fail(e.code, e.what());
+  } catch (const std::bad_alloc&) {
+    return fail(DN_ENOMEM, "host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(DN_EHIP, e.what());
+  } catch (...) {
+    return fail(DN_EHIP, "unknown error");
+  }
+}
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+// Per-device workspace of the cache lookup (partials + result), grown once.
+struct LookupWs {
+  std::mutex mu;
+  std::vector<void*> ws;
+};
+LookupWs g_lookup;
+
+void* lookup_ws(int dev) {
+  std::lock_guard<std::mutex> lk(g_lookup.mu);
+  if ((int)g_lookup.ws.size() <= dev) g_lookup.ws.resize(dev + 1, nullptr);
+  if (!g_lookup.ws[dev]) DN_HIP(hipMalloc(&g_lookup.ws[dev], dn::lookup_workspace_bytes() + 256));
+  return g_lookup.ws[dev];
+}
+
+bool is_dtype(int32_t d) { return d == DN_FP32 || d == DN_BF16; }
+
+}  // namespace
+
+struct dn_handle {
+  dn::Model* m = nullptr;
+};
+
+extern "C" {
+
+dn_status dn_weight_count(const dn_config* cfg, size_t* n_floats) {
+  return guarded([&] {
+    DN_CHECK(cfg && n_floats, "dn_weight_count: null pointer");
+    const auto t = dn::weight_table(*cfg);
+    *n_floats = t.empty() ? 0 : static_cast<size_t>(t.back().offset + t.back().numel);
+  });
+}
+
+dn_status dn_weight_table(const dn_config* cfg, int64_t* numel, int32_t* fan_in, int32_t* kind, size_t capacity,
+                          size_t* n_tensors) {
+  return guarded([&] {
+    DN_CHECK(cfg && n_tensors, "dn_weight_table: null pointer");
+    const auto t = dn::weight_table(*cfg);
+    DN_CHECK(capacity == 0 || capacity >= t.size(), "dn_weight_table: capacity too small");
+    DN_CHECK(capacity == 0 || (numel && fan_in && kind), "dn_weight_table: null output array");
+    if (capacity) {
+      for (size_t i = 0; i < t.size(); ++i) {
+        numel[i] = t[i].numel;
+        fan_in[i] = t[i].fan_in;
+        kind[i] = t[i].kind;
+      }
+    }
+    *n_tensors = t.size();
+  });
+}
+
+dn_status dn_create(const dn_config* cfg, const float* weights, size_t n_floats, int32_t weights_location,
+                    dn_handle** out) {
+  return guarded([&] {
+    DN_CHECK(cfg && weights && out, "dn_create: null pointer");
+    DN_CHECK(weights_location == DN_WEIGHTS_HOST || weights_location == DN_WEIGHTS_DEVICE,
+             "dn_create: bad weights_location");
+    dn::Model* m = dn::model_create(*cfg, weights, n_floats, weights_location == DN_WEIGHTS_DEVICE);
+    dn_handle* h = new dn_handle();
+    h->m = m;
+    *out = h;
+  });
+}
+
+dn_status dn_denoise(dn_handle* h, float* latent, const float* text_ctx, const int32_t* timesteps,
+                     int32_t n_timesteps, int32_t start_step, int32_t n_steps, float cfg_scale, void* stream) {
+  return guarded([&] {
+    DN_CHECK(h && h->m, "dn_denoise: null handle");
+    dn::model_denoise(h->m, latent, text_ctx, timesteps, n_timesteps, start_step, n_steps, cfg_scale,
+                      as_stream(stream));
+  });
+}
+
+dn_status dn_unet_eps(dn_handle* h, const float* x, int32_t t, const float* text_ctx, float cfg_scale, float* out_raw,
+                      float* out_guided, void* stream) {
+  return guarded([&] {
+    DN_CHECK(h && h->m, "dn_unet_eps: null handle");
+    dn::model_unet_eps(h->m, x, t, text_ctx, cfg_scale, out_raw, out_guided, as_stream(stream));
+  });
+}
+
+dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64_t n, int32_t dim, int64_t* out_idx,
+                    float* out_score) {
+  return guarded([&] {
+    DN_CHECK(query_emb && cache_embs && out_idx, "ac_lookup: null pointer");
+    DN_CHECK(n >= 1, "ac_lookup: n must be >= 1");
+    DN_CHECK(dim >= 1, "ac_lookup: dim must be >= 1");
+    int dev = 0;
+    DN_HIP(hipGetDevice(&dev));
+    char* ws = static_cast<char*>(lookup_ws(dev));
+    long long* idx_dev = reinterpret_cast<long long*>(ws + dn::lookup_workspace_bytes());
+    float* score_dev = reinterpret_cast<float*>(ws + dn::lookup_workspace_bytes() + 8);
+    dn::lookup(query_emb, cache_embs, n, dim, ws, idx_dev, score_dev, nullptr);
+    long long idx = -1;
+    float score = 0.f;
+    DN_HIP(hipMemcpy(&idx, idx_dev, sizeof(idx), hipMemcpyDeviceToHost));
+    DN_HIP(hipMemcpy(&score, score_dev, sizeof(score), hipMemcpyDeviceToHost));
+    DN_CHECK(idx >= 0 && idx < n, "ac_lookup: no row scored (zero query or zero-norm cache)");
+    *out_idx = idx;
+    if (out_score) *out_score = score;
+  });
+}
+
+dn_status ac_fetch_latent(const uint16_t* cache_latents, int64_t n, int64_t numel, int64_t idx, float* latent,
+                          void* stream) {
+  return guarded([&] {
+    DN_CHECK(cache_latents && latent, "ac_fetch_latent: null pointer");
+    DN_CHECK(n >= 1 && numel >= 1, "ac_fetch_latent: empty cache");
+    DN_CHECK(idx >= 0 && idx < n, "ac_fetch_latent: index out of range");
+    dn::bf16_latent_to_f32(cache_latents + idx * numel, latent, numel, as_stream(stream));
+  });
+}
+
+dn_status dn_op_linear(int32_t dtype, const void* x, const void* w, const float* bias, const void* resid,
+                       int32_t resid_f32, void* y, int32_t y_f32, int64_t M, int32_t N, int32_t K, int32_t geglu,
+                       void* stream) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_op_linear: bad dtype");
+    DN_CHECK(x && w && y, "dn_op_linear: null pointer");
+    DN_CHECK(M >= 1 && M <= 0x7fffffff && N >= 1 && K >= 1, "dn_op_linear: bad sizes");
+    DN_CHECK(!geglu || N % 32 == 0, "dn_op_linear: GEGLU needs N % 32 == 0");
+    DN_CHECK(!(geglu && resid), "dn_op_linear: GEGLU takes no residual");
+    dn::GemmParams p;
+    p.a0 = x;
+    p.c0 = K;
+    p.lda0 = K;
+    p.taps = 1;
+    p.b = w;
+    p.ldb = K;
+    p.M = static_cast<int>(M);
+    p.N = geglu ? 2 * N : N;
+    p.K = K;
+    p.bias = bias;
+    p.resid = resid;
+    p.ldr = N;
+    p.resid_f32 = resid_f32;
+    p.out = y;
+    p.ldo = N;
+    p.out_f32 = y_f32;
+    p.n_store = N;
+    p.geglu = geglu;
+    if (dtype == DN_BF16)
+      dn::gemm<dn::bf16>(p, as_stream(stream));
+    else
+      dn::gemm<float>(p, as_stream(stream));
+  });
+}
+
+dn_status dn_op_conv3x3(int32_t dtype, const void* x, int32_t n, int32_t H, int32_t W, int32_t Cin, int32_t up,
+                        int32_t stride, const void* w, const float* bias, const float* temb, const void* resid,
+                        void* y, int32_t Cout, int32_t y_f32, void* stream) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_op_conv3x3: bad dtype");
+    DN_CHECK(x && w && y, "dn_op_conv3x3: null pointer");
+    DN_CHECK(n >= 1 && H >= 1 && W >= 1 && Cin >= 1 && Cout >= 1, "dn_op_conv3x3: bad sizes");
+    DN_CHECK(up == 0 || up == 1, "dn_op_conv3x3: up must be 0 or 1");
+    DN_CHECK(stride == 1 || stride == 2, "dn_op_conv3x3: stride must be 1 or 2");
+    const int hl = up ? 2 * H : H, wl = up ? 2 * W : W;
+    const int ho = (hl - 1) / stride + 1, wo = (wl - 1) / stride + 1;
+    dn::GemmParams p;
+    p.a0 = x;
+    p.c0 = Cin;
+    p.lda0 = Cin;
+    p.taps = 9;
+    p.in_h = H;
+    p.in_w = W;
+    p.up = up;
+    p.out_h = ho;
+    p.out_w = wo;
+    p.stride = stride;
+    p.b = w;
+    p.ldb = 9 * Cin;
+    p.M = n * ho * wo;
+    p.N = Cout;
+    p.K = 9 * Cin;
+    p.bias = bias;
+    p.rowvec = temb;
+    p.rowvec_ld = Cout;
+    p.rows_per_sample = ho * wo;
+    p.resid = resid;
+    p.ldr = Cout;
+    p.out = y;
+    p.ldo = Cout;
+    p.out_f32 = y_f32;
+    p.n_store = Cout;
+    if (dtype == DN_BF16)
+      dn::gemm<dn::bf16>(p, as_stream(stream));
+    else
+      dn::gemm<float>(p, as_stream(stream));
+  });
+}
+
+dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void* k, int32_t ldk, const void* v,
+                          int32_t ldv, void* o, int32_t ldo, int32_t B, int32_t heads, int32_t Sq, int32_t Skv,
+                          int32_t head_stride, float scale, void* stream) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_op_attention: bad dtype");
+    DN_CHECK(q && k && v && o, "dn_op_attention: null pointer");
+    DN_CHECK(head_stride == 32 || head_stride == 64, "dn_op_attention: head_stride must be 32 or 64");
+    DN_CHECK(B >= 1 && heads >= 1 && Sq >= 1 && Skv >= 1, "dn_op_attention: bad sizes");
+    DN_CHECK(ldq >= heads * head_stride && ldk >= heads * head_stride && ldv >= heads * head_stride &&
+                 ldo >= heads * head_stride,
+             "dn_op_attention: leading dimension smaller than heads * head_stride");
+    dn::AttnParams a;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.ldq = ldq;
+    a.ldk = ldk;
+    a.ldv = ldv;
+    a.ldo = ldo;
+    a.q_bs = (long long)Sq * ldq;
+    a.kv_bs = (long long)Skv * ldk;
+    DN_CHECK(ldk == ldv, "dn_op_attention: k and v must share a leading dimension");
+    a.o_bs = (long long)Sq * ldo;
+    a.B = B;
+    a.heads = heads;
+    a.Sq = Sq;
+    a.Skv = Skv;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    if (dtype == DN_BF16)
+      dn::attention<dn::bf16>(a, head_stride, as_stream(stream));
+    else
+      dn::attention<float>(a, head_stride, as_stream(stream));
+  });
+}
+
+dn_status dn_op_groupnorm(int32_t dtype, const void* x, void* y, int32_t n, int32_t HW, int32_t C, int32_t G,
+                          const float* gamma, const float* beta, float eps, int32_t silu) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_op_groupnorm: bad dtype");
+    DN_CHECK(x && y && gamma && beta, "dn_op_groupnorm: null pointer");
+    DN_CHECK(n >= 1 && HW >= 1 && C >= 1 && G >= 1 && C % G == 0, "dn_op_groupnorm: bad sizes");
+    float* ws = nullptr;
+    const size_t part = dn::groupnorm_workspace_floats(n, HW, C);
+    DN_HIP(hipMalloc(&ws, (part + (size_t)2 * n * C) * 4));
+    try {
+      dn::GroupNormParams p;
+      p.x0 = x;
+      p.c0 = C;
+      p.n = n;
+      p.HW = HW;
+      p.G = G;
+      p.gamma = gamma;
+      p.beta = beta;
+      p.eps = eps;
+      p.silu = silu;
+      p.y = y;
+      p.partial = ws;
+      p.stats = ws + part;
+      if (dtype == DN_BF16)
+        dn::groupnorm<dn::bf16>(p, nullptr);
+      else
+        dn::groupnorm<float>(p, nullptr);
+      DN_HIP(hipDeviceSynchronize());
+    } catch (...) {
+      (void)hipFree(ws);
+      throw;
+    }
+    DN_HIP(hipFree(ws));
+  });
+}
+
+dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int32_t C, const float* gamma,
+                          const float* beta, float eps, void* stream) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_op_layernorm: bad dtype");
+    DN_CHECK(x && y && gamma && beta, "dn_op_layernorm: null pointer");
+    if (dtype == DN_BF16)
+      dn::layernorm<dn::bf16>(x, static_cast<dn::bf16*>(y), M, C, gamma, beta, eps, as_stream(stream));
+    else
+      dn::layernorm<float>(x, static_cast<float*>(y), M, C, gamma, beta, eps, as_stream(stream));
+  });
+}
+
+void dn_destroy(dn_handle* h) {
+  if (!h) return;
+  dn::model_destroy(h->m);
+  delete h;
+}
+
+const char* dn_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,123 @@
+// Kernel parameter blocks and host launchers (internal to the library).
+#pragma once
+
+#include "common.h"
+
+namespace dn {
+
+// ---------------------------------------------------------------- GEMM / implicit-GEMM conv
+//
+// C[m][n] = sum_k A[m][k] * B[n][k], then the epilogue. B is a packed weight
+// matrix [N][ldb] (K contiguous). A is gathered on the fly:
+//  - linear (taps == 1): row m of the source(s), channels [0, c0) from a0 and
+//    [c0, c0 + c1) from a1 (channel concatenation);
+//  - conv3x3 (taps == 9): NHWC source(s); output pixel m = (s, oy, ox) and
+//    k = tap * (c0 + c1) + c read input pixel (oy*stride + ky - 1, ox*stride + kx - 1)
+//    of the logical input (nearest x2 upsampled when up = 1), zero outside.
+// Epilogue: v = acc + bias[n] + rowvec[m / rows_per_sample][n] + resid[m][n];
+// geglu: columns come in 32-wide (value, gate) block pairs and the output
+// column j of pair p is (acc_v + bias_v) * GELU(acc_g + bias_g).
+struct GemmParams {
+  const void* a0 = nullptr;
+  const void* a1 = nullptr;
+  int c0 = 0, c1 = 0;
+  int lda0 = 0, lda1 = 0;
+  int taps = 1;
+  int in_h = 1, in_w = 1, up = 0;
+  int out_h = 1, out_w = 1, stride = 1;
+  const void* b = nullptr;
+  int ldb = 0;
+  int M = 0, N = 0, K = 0;
+  const float* bias = nullptr;
+  const float* rowvec = nullptr;
+  int rowvec_ld = 0, rows_per_sample = 1;
+  const void* resid = nullptr;
+  int ldr = 0, resid_f32 = 0;
+  void* out = nullptr;
+  int ldo = 0, out_f32 = 0;
+  int n_store = 0;  // output columns written
+  int geglu = 0;
+};
+
+template <typename T> void gemm(const GemmParams& p, hipStream_t s);
+template <typename T> constexpr int gemm_bk() { return sizeof(T) == 2 ? 64 : 32; }
+
+// ---------------------------------------------------------------- attention
+// O = softmax(Q K^T * scale) V per (sample, head). Head h occupies columns
+// [h*D, h*D + D) of q, k, v and o (D = 32 or 64).
+struct AttnParams {
+  const void* q = nullptr;
+  const void* k = nullptr;
+  const void* v = nullptr;
+  void* o = nullptr;
+  int ldq = 0, ldk = 0, ldv = 0, ldo = 0;
+  long long q_bs = 0, kv_bs = 0, o_bs = 0;  // per-sample strides (elements)
+  int B = 0, heads = 0, Sq = 0, Skv = 0;
+  float scale_log2 = 0.f;  // scale * log2(e)
+};
+template <typename T> void attention(const AttnParams& p, int D, hipStream_t s);
+
+// ---------------------------------------------------------------- norms
+// GroupNorm over NHWC [n][HW][c0 + c1] (two channel sources). Statistics in
+// fp32 partial sums merged in fp64; apply writes y (contiguous [n][HW][C]).
+struct GroupNormParams {
+  const void* x0 = nullptr;
+  const void* x1 = nullptr;
+  int c0 = 0, c1 = 0;
+  int n = 0, HW = 0, G = 0;
+  const float* gamma = nullptr;
+  const float* beta = nullptr;
+  float eps = 1e-5f;
+  int silu = 0;
+  void* y = nullptr;
+  float* partial = nullptr;  // workspace, groupnorm_workspace_floats()
+  float* stats = nullptr;    // workspace [2][n][C]: per-channel scale, then shift
+};
+size_t groupnorm_workspace_floats(int n, int HW, int C);
+template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s);
+
+template <typename T>
+void layernorm(const float* x, T* y, long long M, int C, const float* gamma, const float* beta, float eps,
+               hipStream_t s);
+
+// ---------------------------------------------------------------- misc
+void abar_table(double* abar, int T, double beta_start, double beta_end, int schedule, hipStream_t s);
+constexpr int kTsChunk = 256;
+struct TsChunk {
+  int count;
+  int t[kTsChunk];
+};
+// out[s][.] = sinusoidal features of timestep c.t[s], s < c.count (fp64 evaluation)
+void sinusoid(float* out, const TsChunk& c, int dim, hipStream_t s);
+// out[s][j] = sum_k act(in[s][k]) * w[j][k] + b[j] (fp32; act = SiLU if silu)
+void skinny_linear(const float* in, int S, int K, const float* w, const float* b, int J, float* out, int ld_out,
+                   int silu, hipStream_t s);
+template <typename T>
+void latent_to_input(const float* latent, T* xin, int B, int C, int HW, int Cpad, hipStream_t s);
+template <typename T>
+void cfg_ddim(const float* eps, float* latent, T* xin, const double* abar, int t, int t_prev, float scale, int B,
+              int C, int HW, int Cpad, hipStream_t s);
+void export_eps(const float* eps, float* raw, float* guided, float scale, int B, int C, int HW, hipStream_t s);
+template <typename T> void convert_from_f32(const float* src, T* dst, long long n, hipStream_t s);
+void bf16_latent_to_f32(const uint16_t* src, float* dst, long long n, hipStream_t s);
+
+// Weight packing: dst[r][c] (ld_dst) from an fp32 PyTorch-layout source.
+struct PackParams {
+  void* dst = nullptr;
+  int rows = 0, cols = 0, ld_dst = 0;
+  const float* src = nullptr;
+  int row_mode = 0;  // 0 identity, 1 GEGLU interleave, 2 head padding
+  int col_mode = 0;  // 0 identity, 1 head padding, 2 conv3x3 tap-major
+  int src_rows = 0, src_cols = 0;  // source matrix [src_rows][src_cols]
+  int D = 0, Dp = 0;               // head dim and padded head dim
+  int Cin = 0, Cinp = 0;           // conv input channels and padded count
+};
+template <typename T> void pack(const PackParams& p, hipStream_t s);
+void pack_bias(float* dst, int n, const float* src, int src_n, int row_mode, int D, int Dp, hipStream_t s);
+
+// ---------------------------------------------------------------- cache lookup
+size_t lookup_workspace_bytes();
+void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_dev,
+            float* score_dev, hipStream_t s);
+
+}  // namespace dn

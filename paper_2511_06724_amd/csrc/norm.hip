@@ -1,0 +1,248 @@
+// GroupNorm (+SiLU) and LayerNorm kernels (HBM-bound; gfx950).
+//
+// GroupNorm on NHWC activations runs in three launches:
+//   1. partial: each workgroup reduces a chunk of pixels of one sample into
+//      per-channel fp32 sums of x and x^2 (16-byte coalesced loads; a thread
+//      owns one 16-byte channel vector, so its accumulators never mix channels);
+//   2. finalize: one workgroup per (sample, group) merges the chunk partials in
+//      fp64 in a fixed order and writes per-(sample, channel) scale and shift
+//      (gamma * rstd, beta - mean * gamma * rstd);
+//   3. apply: y = x * scale + shift (then SiLU), one FMA per element.
+// The input may be the channel concatenation of two tensors (the up path's
+// [h, skip]); the output is always one contiguous tensor.
+//
+// LayerNorm: one wave per token row in registers, two-pass mean / variance.
+#include "kernels.h"
+
+namespace dn {
+namespace {
+
+constexpr int kPixPerThread = 32;
+
+struct GnGeom {
+  int C, V, vslices, chunks, pix_per_chunk;
+};
+
+template <typename T> GnGeom gn_geom(int HW, int C) {
+  constexpr int VEC = Elem<T>::kVec;
+  GnGeom g;
+  g.C = C;
+  g.V = C / VEC;
+  g.vslices = (g.V + 255) / 256;
+  const int vz = g.V < 256 ? g.V : 256;
+  const int pl = 256 / vz;
+  g.pix_per_chunk = pl * kPixPerThread;
+  g.chunks = (HW + g.pix_per_chunk - 1) / g.pix_per_chunk;
+  return g;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gn_partial_kernel(GroupNormParams p, GnGeom g) {
+  constexpr int VEC = Elem<T>::kVec;
+  __shared__ float red[256 * VEC * 2];
+  const int tid = threadIdx.x;
+  const int chunk = blockIdx.x, n = blockIdx.y, z = blockIdx.z;
+  const int v_begin = z * 256;
+  const int vz = min(g.V - v_begin, 256);
+  const int pl_count = 256 / vz;
+  const int pl = tid / vz;
+  const int vl = tid - pl * vz;
+  const bool active = pl < pl_count;
+
+  float s[VEC], q[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s[e] = q[e] = 0.f;
+  if (active) {
+    int c = (v_begin + vl) * VEC;
+    const T* src;
+    int ld;
+    if (c < p.c0) {
+      src = static_cast<const T*>(p.x0);
+      ld = p.c0;
+    } else {
+      src = static_cast<const T*>(p.x1);
+      ld = p.c1;
+      c -= p.c0;
+    }
+    const int pbeg = chunk * g.pix_per_chunk;
+    const int pend = min(pbeg + g.pix_per_chunk, p.HW);
+    for (int px = pbeg + pl; px < pend; px += pl_count) {
+      const uint4 raw = ld16(src + ((long long)n * p.HW + px) * ld + c);
+      const T* xv = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float x = to_f32(xv[e]);
+        s[e] += x;
+        q[e] += x * x;
+      }
+    }
+  }
+  if (active) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      red[((pl * vz + vl) * VEC + e) * 2 + 0] = s[e];
+      red[((pl * vz + vl) * VEC + e) * 2 + 1] = q[e];
+    }
+  }
+  __syncthreads();
+  for (int j = tid; j < vz * VEC; j += 256) {
+    float ss = 0.f, qq = 0.f;
+    for (int l = 0; l < pl_count; ++l) {
+      ss += red[(l * vz * VEC + j) * 2 + 0];
+      qq += red[(l * vz * VEC + j) * 2 + 1];
+    }
+    const int c = v_begin * VEC + j;
+    float* out = p.partial + (((long long)n * g.chunks + chunk) * g.C + c) * 2;
+    out[0] = ss;
+    out[1] = qq;
+  }
+}
+
+__global__ __launch_bounds__(256) void gn_finalize_kernel(GroupNormParams p, GnGeom g) {
+  __shared__ double rs[256], rq[256];
+  const int tid = threadIdx.x;
+  const int grp = blockIdx.x, n = blockIdx.y;
+  const int cg = g.C / p.G;
+  const int items = g.chunks * cg;
+  double s = 0.0, q = 0.0;
+  for (int i = tid; i < items; i += 256) {
+    const int chunk = i / cg, c = grp * cg + (i - chunk * cg);
+    const float* in = p.partial + (((long long)n * g.chunks + chunk) * g.C + c) * 2;
+    s += in[0];
+    q += in[1];
+  }
+  rs[tid] = s;
+  rq[tid] = q;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w) {
+      rs[tid] += rs[tid + w];
+      rq[tid] += rq[tid + w];
+    }
+    __syncthreads();
+  }
+  const double cnt = (double)cg * p.HW;
+  const double mean = rs[0] / cnt;
+  const double var = fmax(rq[0] / cnt - mean * mean, 0.0);
+  const double rstd = 1.0 / sqrt(var + (double)p.eps);
+  for (int j = tid; j < cg; j += 256) {
+    const int c = grp * cg + j;
+    const double sc = (double)p.gamma[c] * rstd;
+    p.stats[(long long)n * g.C + c] = (float)sc;
+    p.stats[(long long)(p.n + n) * g.C + c] = (float)((double)p.beta[c] - mean * sc);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gn_apply_kernel(GroupNormParams p, GnGeom g) {
+  constexpr int VEC = Elem<T>::kVec;
+  const long long total = (long long)p.n * p.HW * g.V;
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    const long long pix = i / g.V;
+    const int vi = static_cast<int>(i - pix * g.V);
+    const int n = static_cast<int>(pix / p.HW);
+    int c = vi * VEC;
+    const uint4 raw = c < p.c0 ? ld16(static_cast<const T*>(p.x0) + pix * p.c0 + c)
+                               : ld16(static_cast<const T*>(p.x1) + pix * p.c1 + (c - p.c0));
+    const T* xv = reinterpret_cast<const T*>(&raw);
+    const float* sc = p.stats + (long long)n * g.C + c;
+    const float* sh = p.stats + (long long)(p.n + n) * g.C + c;
+    uint4 outv;
+    T* ov = reinterpret_cast<T*>(&outv);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      float v = to_f32(xv[e]) * sc[e] + sh[e];
+      if (p.silu) v = silu_f(v);
+      ov[e] = from_f32<T>(v);
+    }
+    st16(static_cast<T*>(p.y) + pix * g.C + c, outv);
+  }
+}
+
+constexpr int kLnMaxVec = 8;  // float4 vectors per lane: C <= 2048
+
+template <typename T>
+__global__ __launch_bounds__(256) void ln_kernel(const float* x, T* y, long long M, int C, const float* gamma,
+                                                 const float* beta, float eps) {
+  const int lane = threadIdx.x & 63;
+  const long long row = blockIdx.x * 4ll + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const int nv = C / 4;
+  const float4* xr = reinterpret_cast<const float4*>(x + row * C);
+  float4 v[kLnMaxVec];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < kLnMaxVec; ++j) {
+    const int i = lane + 64 * j;
+    if (i < nv) {
+      v[j] = xr[i];
+      s += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+    }
+  }
+  const float mean = wave_sum(s) / C;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < kLnMaxVec; ++j) {
+    const int i = lane + 64 * j;
+    if (i < nv) {
+      const float a = v[j].x - mean, b = v[j].y - mean, c = v[j].z - mean, d = v[j].w - mean;
+      q += (a * a + b * b) + (c * c + d * d);
+    }
+  }
+  const float rstd = rsqrtf(wave_sum(q) / C + eps);
+  T* yr = y + row * C;
+#pragma unroll
+  for (int j = 0; j < kLnMaxVec; ++j) {
+    const int i = lane + 64 * j;
+    if (i < nv) {
+      const int c = 4 * i;
+      yr[c + 0] = from_f32<T>((v[j].x - mean) * rstd * gamma[c + 0] + beta[c + 0]);
+      yr[c + 1] = from_f32<T>((v[j].y - mean) * rstd * gamma[c + 1] + beta[c + 1]);
+      yr[c + 2] = from_f32<T>((v[j].z - mean) * rstd * gamma[c + 2] + beta[c + 2]);
+      yr[c + 3] = from_f32<T>((v[j].w - mean) * rstd * gamma[c + 3] + beta[c + 3]);
+    }
+  }
+}
+
+}  // namespace
+
+size_t groupnorm_workspace_floats(int n, int HW, int C) {
+  // Sized for the smaller vector width (fp32 -> 4 channels per vector -> more pixel lanes).
+  const GnGeom g = gn_geom<float>(HW, C);
+  const GnGeom g2 = gn_geom<bf16>(HW, C);
+  const int chunks = g.chunks > g2.chunks ? g.chunks : g2.chunks;
+  return size_t(n) * chunks * C * 2;
+}
+
+template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int C = p.c0 + p.c1;
+  DN_CHECK(p.n >= 1 && p.HW >= 1 && C >= 1 && p.G >= 1, "groupnorm: empty problem");
+  DN_CHECK(C % p.G == 0, "groupnorm: channels must divide into groups");
+  DN_CHECK(p.c0 % VEC == 0 && p.c1 % VEC == 0, "groupnorm: channel counts must be multiples of 16 bytes");
+  DN_CHECK(p.x0 && p.y && p.partial && p.stats && p.gamma && p.beta && (p.c1 == 0 || p.x1), "groupnorm: null");
+  const GnGeom g = gn_geom<T>(p.HW, C);
+  hipLaunchKernelGGL(gn_partial_kernel<T>, dim3(g.chunks, p.n, g.vslices), dim3(256), 0, s, p, g);
+  hipLaunchKernelGGL(gn_finalize_kernel, dim3(p.G, p.n), dim3(256), 0, s, p, g);
+  const long long total = (long long)p.n * p.HW * g.V;
+  const int blocks = static_cast<int>(total / 256 + 1 < 8192 ? total / 256 + 1 : 8192);
+  hipLaunchKernelGGL(gn_apply_kernel<T>, dim3(blocks), dim3(256), 0, s, p, g);
+  DN_HIP(hipGetLastError());
+}
+
+template <typename T>
+void layernorm(const float* x, T* y, long long M, int C, const float* gamma, const float* beta, float eps,
+               hipStream_t s) {
+  DN_CHECK(M >= 1 && C >= 4 && C % 4 == 0 && C <= 4 * 64 * kLnMaxVec, "layernorm: C must be a multiple of 4, <= 2048");
+  DN_CHECK(x && y && gamma && beta, "layernorm: null");
+  hipLaunchKernelGGL(ln_kernel<T>, dim3(static_cast<unsigned>((M + 3) / 4)), dim3(256), 0, s, x, y, M, C, gamma,
+                     beta, eps);
+  DN_HIP(hipGetLastError());
+}
+
+template void groupnorm<float>(const GroupNormParams&, hipStream_t);
+template void groupnorm<bf16>(const GroupNormParams&, hipStream_t);
+template void layernorm<float>(const float*, float*, long long, int, const float*, const float*, float, hipStream_t);
+template void layernorm<bf16>(const float*, bf16*, long long, int, const float*, const float*, float, hipStream_t);
+
+}  // namespace dn

@@ -1,0 +1,110 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every
+function include/argus_dn.h declares, describes the same canonical weight table as
+the oracle's independent topology generator, and rejects bad arguments before
+touching the device."""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import topology as T
+from paper_2511_06724_amd import dn, workloads as W
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "argus_dn.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:dn_status|void|const char\*)\s+(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared()
+    assert "dn_create" in names and "ac_lookup" in names and "dn_denoise" in names
+    for n in names:
+        assert hasattr(dn.lib, n), n
+    assert sorted(dn.EXPORTED) == names
+
+
+KIND = {"w": 0, "b": 1, "g": 2, "beta": 3}
+
+
+@pytest.mark.parametrize("make", [W.tiny, W.sd15_level, W.sdxl, W.sdxl_small, W.sd20_shape])
+def test_weight_table_matches_oracle(make):
+    cfg = make()
+    ours = dn.weight_table(cfg)
+    ref = [(int(np.prod(s)), f, KIND[k]) for _, s, k, f in T.tensor_table(cfg)]
+    assert ours == ref
+    assert dn.weight_count(cfg) == T.param_count(cfg)
+
+
+def _expect(code, fn, *args):
+    with pytest.raises(dn.DnError) as e:
+        fn(*args)
+    assert e.value.code == code
+    return str(e.value)
+
+
+@pytest.mark.parametrize("change,msg", [
+    (dict(levels=((320, 1, 8, 41), (640, 1, 10, 64))), "heads * head_dim"),
+    (dict(latent_h=63), "divisible"),
+    (dict(model_channels=100), "multiple of 64"),
+    (dict(batch=0), "batch"),
+    (dict(dtype=7), "dtype"),
+    (dict(gn_groups=7), "divisible by gn_groups"),
+    (dict(ctx_dim=100), "ctx_dim"),
+    (dict(beta_schedule=3), "beta_schedule"),
+])
+def test_invalid_configs_rejected(change, msg):
+    cfg = W.sd15_level().with_(**change)
+    text = _expect(dn.DN_EINVAL, dn.weight_count, cfg)
+    assert msg in text
+
+
+def test_abi_version_checked():
+    c = dn.to_c_config(W.tiny())
+    c.abi_version = 99
+    n = C.c_size_t(123)
+    assert dn.lib.dn_weight_count(C.byref(c), C.byref(n)) == dn.DN_EINVAL
+    assert n.value == 123
+    assert b"abi_version" in dn.lib.dn_last_error()
+
+
+def test_null_and_range_errors_touch_nothing():
+    # weight table capacity too small
+    c = dn.to_c_config(W.tiny())
+    nt = C.c_size_t(0)
+    a = np.zeros(3, np.int64)
+    b = np.zeros(3, np.int32)
+    k = np.zeros(3, np.int32)
+    assert dn.lib.dn_weight_table(C.byref(c), a.ctypes.data, b.ctypes.data, k.ctypes.data, 3, C.byref(nt)) == -1
+    # lookup: null pointers, n <= 0, dim <= 0 -> DN_EINVAL and out_idx untouched (checked before any HIP call)
+    for q, cache, n, dim in [(None, 1, 5, 8), (1, None, 5, 8), (1, 1, 0, 8), (1, 1, 5, 0), (1, 1, -3, 8)]:
+        code, idx, _ = dn.ac_lookup_raw(q, cache, n, dim)
+        assert code == dn.DN_EINVAL and idx == -7
+    # denoise / unet hooks with a null handle
+    assert dn.lib.dn_denoise(None, None, None, None, 0, 0, 0, 7.5, None) == dn.DN_EINVAL
+    assert dn.lib.dn_unet_eps(None, None, 0, None, 7.5, None, None, None) == dn.DN_EINVAL
+    # create: blob length mismatch is rejected before any device work
+    blob = np.zeros(10, np.float32)
+    h = C.c_void_p()
+    assert dn.lib.dn_create(C.byref(c), blob.ctypes.data, 10, 0, C.byref(h)) == dn.DN_EINVAL
+    assert b"weight blob" in dn.lib.dn_last_error()
+    assert h.value is None
+    # op entry points validate before launching
+    assert dn.lib.dn_op_linear(5, 1, 1, None, None, 0, 1, 0, 4, 4, 64, 0, None) == dn.DN_EINVAL
+    assert dn.lib.dn_op_attention(1, 1, 64, 1, 64, 1, 64, 1, 64, 1, 1, 4, 4, 48, 0.1, None) == dn.DN_EINVAL
+    assert dn.lib.dn_op_conv3x3(1, 1, 1, 4, 4, 64, 2, 1, 1, None, None, None, 1, 8, 0, None) == dn.DN_EINVAL
+    assert dn.lib.ac_fetch_latent(1, 4, 16, 4, 1, None) == dn.DN_EINVAL
+    dn.lib.dn_destroy(None)
+
+
+def test_one_hip_runtime_per_process():
+    """The library binds to the HIP runtime PyTorch already loaded (one runtime per
+    process, so torch streams and allocations are valid in the library)."""
+    maps = {l.split()[-1] for l in open("/proc/self/maps") if "libamdhip64" in l}
+    assert len(maps) == 1, maps

@@ -1,0 +1,184 @@
+"""Denoise-loop parity on the GPU through dn_create / dn_unet_eps / dn_denoise.
+
+Bars (relative L2 over the whole tensor, oracle = reference):
+* fp32 mode, one iteration (teacher-forced: the oracle's latent goes in):
+  UNet output, guided eps and the DDIM update within 1e-4;
+* bf16 mode, one iteration: UNet output within 2e-2;
+* bf16 mode, the tiny denoiser's free-running 10-step trajectory: final latent
+  within 5e-2;
+* resuming at step k (approximate caching, Sec. 2.1) is bitwise equal to the
+  uninterrupted run, and every result is bitwise reproducible.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import sampler, schedule as S, unet
+from paper_2511_06724_amd import dn, workloads as W
+from tests.gpu_util import DEV, announce, f32_dev, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+_CACHE = {}
+
+
+def _model(cfg, seed=42):
+    key = (repr(cfg), seed)
+    if key not in _CACHE:
+        blob = W.weight_blob(dn.weight_table(cfg), seed)
+        _CACHE.clear()
+        _CACHE[key] = (dn.Denoiser(cfg, blob), unet.unpack(cfg, blob))
+    return _CACHE[key]
+
+
+def _eps(model, cfg, x, t, ctx, scale):
+    raw = torch.empty((2 * cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device=DEV)
+    guided = torch.empty((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device=DEV)
+    model.unet_eps(f32_dev(x), t, f32_dev(ctx), scale, raw, guided)
+    torch.cuda.synchronize()
+    return raw.cpu().numpy(), guided.cpu().numpy()
+
+
+@pytest.mark.parametrize("t", [901, 501, 1])
+def test_tiny_fp32_step(t):
+    announce(f"tiny fp32 step t={t}")
+    cfg = W.tiny(W.DN_FP32)
+    model, Wt = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    raw, guided = _eps(model, cfg, x, t, ctx, 7.5)
+    ref_raw, ref_eps, ref_next = sampler.step(cfg, Wt, x, ctx, t, t - 100 if t > 100 else -1, 7.5)
+    assert rel_l2(raw, ref_raw) <= 1e-4
+    assert rel_l2(guided, ref_eps) <= 1e-4
+    lat = f32_dev(x)
+    ts = np.array([t, t - 100 if t > 100 else -1], np.int32)
+    model.denoise(lat, f32_dev(ctx), ts, 0, 1, 7.5)
+    torch.cuda.synchronize()
+    assert rel_l2(lat.cpu().numpy(), ref_next) <= 1e-4
+
+
+def test_tiny_fp32_trajectory_and_batch2():
+    announce("tiny fp32 trajectory, batch 2")
+    cfg = W.tiny(W.DN_FP32).with_(batch=2)
+    model, Wt = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    ts = S.default_timesteps(10)
+    ref = sampler.denoise(cfg, Wt, x, ctx, ts, 0, 10, 7.5)
+    lat = f32_dev(x)
+    model.denoise(lat, f32_dev(ctx), ts, 0, 10, 7.5)
+    torch.cuda.synchronize()
+    assert rel_l2(lat.cpu().numpy(), ref) <= 1e-3
+
+
+def test_tiny_bf16_teacher_forced_steps_and_trajectory():
+    announce("tiny bf16 teacher-forced steps + 10-step trajectory")
+    cfg = W.tiny(W.DN_BF16)
+    model, Wt = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    ts = S.default_timesteps(10)
+    trace = []
+    ref_final = sampler.denoise(cfg, Wt, x, ctx, ts, 0, 10, 7.5, trace=trace)
+    xs = [x] + trace[:-1]
+    worst = 0.0
+    for i in range(10):
+        raw, _ = _eps(model, cfg, xs[i], int(ts[i]), ctx, 7.5)
+        ref_raw, _, _ = sampler.step(cfg, Wt, xs[i], ctx, int(ts[i]), int(ts[i + 1]), 7.5)
+        worst = max(worst, rel_l2(raw, ref_raw))
+    announce(f"  worst per-step rel-L2 {worst:.3e}")
+    assert worst <= 2e-2
+    lat = f32_dev(x)
+    model.denoise(lat, f32_dev(ctx), ts, 0, 10, 7.5)
+    torch.cuda.synchronize()
+    e = rel_l2(lat.cpu().numpy(), ref_final)
+    announce(f"  final latent rel-L2 {e:.3e}")
+    assert e <= 5e-2
+
+
+@pytest.mark.parametrize("dtype", [W.DN_FP32, W.DN_BF16])
+def test_resume_is_bitwise_and_deterministic(dtype):
+    announce(f"resume/determinism dtype={dtype}")
+    cfg = W.tiny(dtype)
+    model, _ = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    ts = S.default_timesteps(10)
+    cd = f32_dev(ctx)
+    a = f32_dev(x)
+    model.denoise(a, cd, ts, 0, 10, 7.5)
+    b = f32_dev(x)
+    model.denoise(b, cd, ts, 0, 4, 7.5)
+    model.denoise(b, cd, ts, 4, 6, 7.5)
+    c = f32_dev(x)
+    model.denoise(c, cd, ts, 0, 10, 7.5)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert torch.equal(a, c)
+    # n_steps = 0 is a no-op
+    d = a.clone()
+    model.denoise(d, cd, ts, 10, 0, 7.5)
+    torch.cuda.synchronize()
+    assert torch.equal(a, d)
+
+
+def test_denoise_argument_errors_leave_latent_untouched():
+    cfg = W.tiny(W.DN_FP32)
+    model, _ = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    lat = f32_dev(x)
+    before = lat.clone()
+    ts = S.default_timesteps(10)
+    for args in [(ts, 5, 6), (ts, -1, 2), (np.array([901, 2000, -1], np.int32), 0, 2)]:
+        with pytest.raises(dn.DnError) as e:
+            model.denoise(lat, f32_dev(ctx), args[0], args[1], args[2], 7.5)
+        assert e.value.code == dn.DN_EINVAL
+    torch.cuda.synchronize()
+    assert torch.equal(lat, before)
+
+
+def test_sd15_level_bf16_step():
+    """Two-level SD-1.5-shaped UNet (64x64 latent, d = 40 heads padded to 64 on the
+    GPU only, skip concatenations, middle block): one teacher-forced iteration."""
+    announce("sd15-level bf16 step (oracle ~1.2 TFLOP on the CPU)")
+    cfg = W.sd15_level(W.DN_BF16)
+    model, Wt = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    raw, _ = _eps(model, cfg, x, 981, ctx, 7.5)
+    ref_raw, _, _ = sampler.step(cfg, Wt, x, ctx, 981, 961, 7.5)
+    e = rel_l2(raw, ref_raw)
+    announce(f"  rel-L2 {e:.3e}")
+    assert e <= 2e-2
+
+
+def test_sdxl_step_properties():
+    """Full SD-XL shapes (2.56 B parameters, 128x128 latent, batch 2 with guidance):
+    outputs finite and bitwise reproducible, resume at k bitwise equal to the full run."""
+    announce("sdxl properties: finite, deterministic, resume")
+    cfg = W.sdxl(W.DN_BF16)
+    _CACHE.clear()
+    g = torch.Generator(device=DEV).manual_seed(11)
+    table = dn.weight_table(cfg)
+    n = sum(t[0] for t in table)
+    blob = torch.empty(n, device=DEV)
+    off = 0
+    for numel, fan, kind in table:
+        v = blob[off:off + numel]
+        if kind in (0, 1):
+            v.normal_(0.0, fan ** -0.5, generator=g)
+        elif kind == 2:
+            v.normal_(1.0, 0.1, generator=g)
+        else:
+            v.normal_(0.0, 0.1, generator=g)
+        off += numel
+    model = dn.Denoiser(cfg, blob)
+    del blob
+    x = torch.randn((1, 4, 128, 128), device=DEV, generator=g)
+    ctx = torch.randn((2, 77, 2048), device=DEV, generator=g)
+    ts = S.default_timesteps(50)
+    a = x.clone()
+    model.denoise(a, ctx, ts, 0, 3, 7.5)
+    b = x.clone()
+    model.denoise(b, ctx, ts, 0, 1, 7.5)
+    model.denoise(b, ctx, ts, 1, 2, 7.5)
+    torch.cuda.synchronize()
+    assert torch.isfinite(a).all()
+    assert torch.equal(a, b)
+    model.close()

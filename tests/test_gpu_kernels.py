@@ -1,0 +1,254 @@
+"""Kernel parity on the GPU: each single-kernel entry point of the C ABI against the
+oracle's layer on the same seeded inputs (the inputs the kernel sees, i.e. after
+rounding to the kernel dtype, are what the oracle receives, in fp64).
+
+Tolerances (relative L2 over the whole output):
+* fp32 kernels: 1e-5 (fp32 accumulation over K <= 23040 terms, different order);
+* bf16 kernels: 8e-3 — fp32 accumulation, but the output itself is rounded to
+  bf16 (relative error <= 2^-9 = 2e-3 per element) and attention rounds P to bf16;
+  fp32 outputs of bf16 kernels: 2e-3.
+Shapes span several tiles with ragged M, N and sequence tails; the last tests run
+the SD-XL shapes of the benchmark in the same launch configuration and compare
+sampled outputs computed one by one.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import layers as L
+from paper_2511_06724_amd import dn
+from tests.gpu_util import DEV, announce, f32_dev, host, rel_l2, tdtype, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL = {dn.DN_FP32: 1e-5, dn.DN_BF16: 8e-3}
+DT = [dn.DN_FP32, dn.DN_BF16]
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280)])
+def test_linear(dtype, M, N, K):
+    announce(f"linear dtype={dtype} M={M} N={N} K={K}")
+    r = _rng(M + N + K)
+    x, xh = to_dev(r.standard_normal((M, K)), dtype)
+    w, wh = to_dev(r.standard_normal((N, K)) / math.sqrt(K), dtype)
+    b = r.standard_normal(N).astype(np.float32)
+    res = r.standard_normal((M, N)).astype(np.float32)
+    y = torch.empty((M, N), device=DEV, dtype=tdtype(dtype))
+    dn.op_linear(dtype, x, w, f32_dev(b), y, M, N, K)
+    yr = torch.empty((M, N), device=DEV, dtype=torch.float32)
+    dn.op_linear(dtype, x, w, f32_dev(b), yr, M, N, K, resid=f32_dev(res), resid_f32=True, y_f32=True)
+    torch.cuda.synchronize()
+    ref = L.linear(xh, wh, b.astype(np.float64))
+    assert rel_l2(host(y), ref) < TOL[dtype]
+    assert rel_l2(host(yr), ref + res) < (1e-5 if dtype == dn.DN_FP32 else 2e-3)
+
+
+def _interleave(w1, n):
+    """GEGLU packed layout: 32-row blocks alternate value rows and gate rows."""
+    out = np.empty_like(w1)
+    for j in range(n // 32):
+        out[64 * j:64 * j + 32] = w1[32 * j:32 * j + 32]
+        out[64 * j + 32:64 * j + 64] = w1[n + 32 * j:n + 32 * j + 32]
+    return out
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("M,N,K", [(300, 96, 128), (512, 1280, 320)])
+def test_linear_geglu(dtype, M, N, K):
+    announce(f"geglu dtype={dtype} M={M} N={N} K={K}")
+    r = _rng(7 * M + N)
+    x, xh = to_dev(r.standard_normal((M, K)), dtype)
+    w1 = (r.standard_normal((2 * N, K)) / math.sqrt(K)).astype(np.float32)
+    b1 = r.standard_normal(2 * N).astype(np.float32)
+    wp, _ = to_dev(_interleave(w1, N), dtype)
+    w1h = host(to_dev(w1, dtype)[0])
+    bp = _interleave(b1[:, None], N)[:, 0].copy()
+    y = torch.empty((M, N), device=DEV, dtype=tdtype(dtype))
+    dn.op_linear(dtype, x, wp, f32_dev(bp), y, M, N, K, geglu=True)
+    torch.cuda.synchronize()
+    u = L.linear(xh, w1h, b1.astype(np.float64))
+    ref = u[:, :N] * L.gelu(u[:, N:])
+    assert rel_l2(host(y), ref) < TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("n,H,W,Cin,Cout,up,stride", [
+    (2, 9, 7, 64, 96, 0, 1), (2, 9, 7, 64, 96, 0, 2), (1, 5, 6, 128, 64, 1, 1), (2, 16, 16, 128, 320, 0, 1)])
+def test_conv3x3(dtype, n, H, W, Cin, Cout, up, stride):
+    announce(f"conv dtype={dtype} n={n} H={H} W={W} Cin={Cin} Cout={Cout} up={up} stride={stride}")
+    r = _rng(n * H * W + Cin + Cout + up + stride)
+    x, xh = to_dev(r.standard_normal((n, H, W, Cin)), dtype)
+    wt = (r.standard_normal((Cout, Cin, 3, 3)) / math.sqrt(9 * Cin)).astype(np.float32)
+    wd, _ = to_dev(wt.transpose(0, 2, 3, 1), dtype)
+    wh = host(to_dev(wt, dtype)[0])
+    b = r.standard_normal(Cout).astype(np.float32)
+    temb = r.standard_normal((n, Cout)).astype(np.float32)
+    xin = xh.transpose(0, 3, 1, 2)
+    if up:
+        xin = L.upsample_nearest2x(xin)
+    ref = L.conv2d(xin, wh, b.astype(np.float64), stride=stride)          # NCHW
+    ho, wo = ref.shape[2], ref.shape[3]
+    res = r.standard_normal((n, ho, wo, Cout)).astype(np.float32)
+    resd, resh = to_dev(res, dtype)
+    y = torch.empty((n, ho, wo, Cout), device=DEV, dtype=tdtype(dtype))
+    dn.op_conv3x3(dtype, x, n, H, W, Cin, wd, f32_dev(b), y, Cout, up=up, stride=stride, temb=f32_dev(temb),
+                  resid=resd)
+    torch.cuda.synchronize()
+    full = ref.transpose(0, 2, 3, 1) + temb[:, None, None, :] + resh
+    assert rel_l2(host(y), full) < TOL[dtype]
+
+
+def _pad_heads(a, heads, d, dp):
+    """[.., heads*d] -> [.., heads*dp] with zeros in each head's padding columns."""
+    out = np.zeros(a.shape[:-1] + (heads * dp,), dtype=a.dtype)
+    for h in range(heads):
+        out[..., h * dp:h * dp + d] = a[..., h * d:(h + 1) * d]
+    return out
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("B,heads,Sq,Skv,d", [(2, 3, 200, 77, 64), (1, 2, 256, 300, 64), (2, 2, 130, 96, 40),
+                                              (2, 4, 256, 256, 16), (1, 1, 5, 1, 64)])
+def test_attention(dtype, B, heads, Sq, Skv, d):
+    announce(f"attention dtype={dtype} B={B} heads={heads} Sq={Sq} Skv={Skv} d={d}")
+    r = _rng(B * heads + Sq + Skv + d)
+    dp = 32 if d <= 32 else 64
+    q = r.standard_normal((B, Sq, heads * d)).astype(np.float32)
+    k = r.standard_normal((B, Skv, heads * d)).astype(np.float32)
+    v = r.standard_normal((B, Skv, heads * d)).astype(np.float32)
+    qd, qh = to_dev(_pad_heads(q, heads, d, dp), dtype)
+    kd, kh = to_dev(_pad_heads(k, heads, d, dp), dtype)
+    vd, vh = to_dev(_pad_heads(v, heads, d, dp), dtype)
+    o = torch.zeros((B, Sq, heads * dp), device=DEV, dtype=tdtype(dtype))
+    P = heads * dp
+    dn.op_attention(dtype, qd, P, kd, P, vd, P, o, P, B, heads, Sq, Skv, dp, 1.0 / math.sqrt(d))
+    torch.cuda.synchronize()
+    # oracle: multi-head attention with identity projections on the unpadded heads
+    strip = lambda a: np.concatenate([a[..., h * dp:h * dp + d] for h in range(heads)], axis=-1)
+    c = heads * d
+    eye, zero = np.eye(c), np.zeros((c, c))
+    xkv = np.concatenate([strip(kh), strip(vh)], axis=-1)          # K and V from one [.., 2c] input
+    ref = L.attention(strip(qh), xkv, eye, np.hstack([eye, zero]), np.hstack([zero, eye]), eye, np.zeros(c), heads)
+    got = host(o)
+    assert rel_l2(strip(got), ref) < TOL[dtype]
+    # padding columns of o are zero (v's padding is zero)
+    if dp != d:
+        assert np.all(got[..., d:dp] == 0)
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("n,HW,C,G,silu", [(2, 300, 320, 32, 1), (2, 64, 64, 32, 0), (1, 1000, 1920, 32, 1)])
+def test_groupnorm(dtype, n, HW, C, G, silu):
+    announce(f"groupnorm dtype={dtype} n={n} HW={HW} C={C} silu={silu}")
+    r = _rng(n + HW + C)
+    x, xh = to_dev(0.5 + 2.0 * r.standard_normal((n, HW, C)), dtype)
+    g = (1 + 0.1 * r.standard_normal(C)).astype(np.float32)
+    b = (0.1 * r.standard_normal(C)).astype(np.float32)
+    y = torch.empty((n, HW, C), device=DEV, dtype=tdtype(dtype))
+    dn.op_groupnorm(dtype, x, y, n, HW, C, G, f32_dev(g), f32_dev(b), 1e-5, silu)
+    ref = L.group_norm(xh.transpose(0, 2, 1)[..., None], G, g.astype(np.float64), b.astype(np.float64), 1e-5)
+    ref = ref[..., 0].transpose(0, 2, 1)
+    if silu:
+        ref = L.silu(ref)
+    assert rel_l2(host(y), ref) < (2e-6 if dtype == dn.DN_FP32 else TOL[dtype])
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("M,C", [(300, 1280), (77, 64), (2048, 640)])
+def test_layernorm(dtype, M, C):
+    announce(f"layernorm dtype={dtype} M={M} C={C}")
+    r = _rng(M + C)
+    x = (1.0 + 3.0 * r.standard_normal((M, C))).astype(np.float32)
+    g = (1 + 0.1 * r.standard_normal(C)).astype(np.float32)
+    b = (0.1 * r.standard_normal(C)).astype(np.float32)
+    y = torch.empty((M, C), device=DEV, dtype=tdtype(dtype))
+    dn.op_layernorm(dtype, f32_dev(x), y, M, C, f32_dev(g), f32_dev(b), 1e-5)
+    torch.cuda.synchronize()
+    ref = L.layer_norm(x.astype(np.float64), g.astype(np.float64), b.astype(np.float64), 1e-5)
+    assert rel_l2(host(y), ref) < (2e-6 if dtype == dn.DN_FP32 else TOL[dtype])
+
+
+# ----------------------------------------------------------------------------- SD-XL shapes, sampled
+
+def _sample_idx(r, shape, count):
+    return tuple(r.integers(0, s, size=count) for s in shape)
+
+
+def test_sdxl_ff_in_geglu_sampled():
+    """FF-in of a 32x32 SD-XL transformer block: 2048 x (2 x 5120) x 1280, bf16, GEGLU epilogue."""
+    announce("sdxl ff-in geglu 2048x10240x1280")
+    M, N, K = 2048, 5120, 1280
+    g = torch.Generator(device=DEV).manual_seed(3)
+    x = torch.randn((M, K), device=DEV, generator=g).to(torch.bfloat16)
+    w = (torch.randn((2 * N, K), device=DEV, generator=g) / math.sqrt(K)).to(torch.bfloat16)
+    b = torch.randn(2 * N, device=DEV, generator=g)
+    y = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+    dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True)
+    torch.cuda.synchronize()
+    r = _rng(5)
+    ms, ns = _sample_idx(r, (M, N), 512)
+    xh, wh, bh, yh = host(x), host(w), host(b), host(y)
+    for m, n in zip(ms, ns):
+        blk, c = n // 32, n % 32
+        rv, rg = 64 * blk + c, 64 * blk + 32 + c
+        a = float(xh[m] @ wh[rv] + bh[rv])
+        gg = float(xh[m] @ wh[rg] + bh[rg])
+        ref = a * 0.5 * gg * (1 + math.erf(gg / math.sqrt(2)))
+        assert abs(yh[m, n] - ref) <= 1e-2 * max(1.0, abs(ref)), (m, n, yh[m, n], ref)
+
+
+def test_sdxl_conv_top_level_sampled():
+    """3x3 conv at the SD-XL top level: 2 x 128 x 128 x 320 -> 320 (M = 32768, K = 2880), bf16."""
+    announce("sdxl conv 32768x320x2880")
+    n, H, W, C = 2, 128, 128, 320
+    g = torch.Generator(device=DEV).manual_seed(4)
+    x = torch.randn((n, H, W, C), device=DEV, generator=g).to(torch.bfloat16)
+    w = (torch.randn((C, 3, 3, C), device=DEV, generator=g) / math.sqrt(9 * C)).to(torch.bfloat16)
+    b = torch.randn(C, device=DEV, generator=g)
+    y = torch.empty((n, H, W, C), device=DEV, dtype=torch.bfloat16)
+    dn.op_conv3x3(dn.DN_BF16, x, n, H, W, C, w, b, y, C)
+    torch.cuda.synchronize()
+    r = _rng(6)
+    xh, wh, bh, yh = host(x), host(w), host(b), host(y)
+    for s, yy, xx, co in zip(*_sample_idx(r, (n, H, W, C), 256)):
+        acc = bh[co]
+        for ky in range(3):
+            for kx in range(3):
+                iy, ix = yy + ky - 1, xx + kx - 1
+                if 0 <= iy < H and 0 <= ix < W:
+                    acc += float(xh[s, iy, ix] @ wh[co, ky, kx])
+        assert abs(yh[s, yy, xx, co] - acc) <= 1e-2 * max(1.0, abs(acc)), (s, yy, xx, co)
+
+
+def test_sdxl_self_attention_sampled():
+    """Self-attention at the SD-XL 64x64 level: 2 samples x 10 heads, S = 4096, d = 64, bf16."""
+    announce("sdxl attention S=4096 10x64")
+    B, heads, S, d = 2, 10, 4096, 64
+    P = heads * d
+    g = torch.Generator(device=DEV).manual_seed(5)
+    qkv = torch.randn((B, S, 3 * P), device=DEV, generator=g).to(torch.bfloat16)
+    o = torch.empty((B, S, P), device=DEV, dtype=torch.bfloat16)
+    q, k, v = qkv[..., :P], qkv[..., P:2 * P], qkv[..., 2 * P:]
+    dn.lib.dn_op_attention(dn.DN_BF16, q.data_ptr(), 3 * P, k.data_ptr(), 3 * P, v.data_ptr(), 3 * P, o.data_ptr(),
+                           P, B, heads, S, S, 64, 1.0 / 8.0, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    r = _rng(7)
+    qh = host(qkv)
+    oh = host(o)
+    for b, h in [(0, 0), (1, 9), (0, 5)]:
+        rows = r.integers(0, S, size=16)
+        K_ = qh[b, :, P + h * d:P + (h + 1) * d]
+        V_ = qh[b, :, 2 * P + h * d:2 * P + (h + 1) * d]
+        for i in rows:
+            s = K_ @ qh[b, i, h * d:(h + 1) * d] / 8.0
+            p = np.exp(s - s.max())
+            ref = (p / p.sum()) @ V_
+            assert rel_l2(oh[b, i, h * d:(h + 1) * d], ref) < 1e-2, (b, h, i)
