@@ -114,7 +114,7 @@ def roofline_ff_in(torch, dn, stream, iters=20):
     avg_s = e0.elapsed_time(e1) / 1e3 / iters
     flops = 2.0 * M * (2 * N) * K
     achieved = flops / avg_s / 1e12
-    return {"kernel": "gemm_kernel<bf16,256,linear> FF-in GEGLU 2048x10240x1280", "bound": "mfma",
+    return {"kernel": "gemm_kernel<bf16,128x128,linear> FF-in GEGLU 2048x10240x1280", "bound": "mfma",
             "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
             "avg_launch_us": round(avg_s * 1e6, 2), "flops_per_launch": flops}

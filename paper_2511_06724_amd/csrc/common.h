@@ -52,6 +52,17 @@ template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return sta
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
 
+// Exact-form GELU, x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf from
+// Abramowitz & Stegun (1964) formula 7.1.26: |error| <= 1.5e-7 on the real line
+// (one reciprocal, one exponential, five FMAs instead of a library erf).
+__device__ __forceinline__ float gelu_erf(float x) {
+  const float z = fabsf(x) * 0.70710678118654752f;
+  const float t = __frcp_rn(1.0f + 0.3275911f * z);
+  const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float e = 1.0f - poly * __expf(-z * z);  // erf(|x| / sqrt 2)
+  return 0.5f * x * (1.0f + copysignf(e, x));
+}
+
 // 16-byte vector load/store helpers.
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }

@@ -6,37 +6,122 @@
 // 1x1 skip convolutions and every linear layer of the transformer blocks
 // (fused QKV, attention outputs, GEGLU feed-forward, projections).
 //
-// Tiling: 256 threads = 4 waves in a 2x2 grid; block tile BM x 128, wave tile
-// (BM/2) x 64 built from 32x32 MFMA blocks; K step BK = 128 bytes of each row
-// (64 bf16 / 32 fp32), staged through double-buffered LDS with one barrier per
-// K step. Rows of A and B beyond M / N are clamped on load and masked on store.
+// Tiling: 256 threads = 4 waves in a 2x2 grid; block tile BM x BN in
+// {256x128, 128x256, 128x128}, wave tile (BM/2) x (BN/2) built from 32x32x16 MFMA blocks; K
+// step BK = 128 bytes of each row (64 bf16 / 32 fp32), staged through
+// double-buffered LDS (one barrier per K step; the next tile's global loads are
+// issued a full K step ahead). The MFMA is issued as C^T = B A^T so that each
+// lane holds four consecutive output columns of one row: the epilogue stores
+// 8 (bf16) or 16 (fp32) contiguous bytes per lane and reads bias / residual as
+// vectors. Rows of A and B beyond M / N are clamped on load and masked on store.
+//
+// Work distribution: tiles are numbered so that each XCD (consecutive
+// workgroup ids go round-robin over the 8 XCDs) works through a contiguous band
+// of output columns with all row tiles, keeping that band of B in its L2.
+// Optional split-K: each of S workgroups of a tile reduces a K range into fp32
+// partials; the last one to arrive (integer atomic counter per tile) sums the S
+// partials in split order and runs the epilogue, so the result does not depend
+// on arrival order. The counter is reset by that workgroup.
 #include "kernels.h"
 
 namespace dn {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBN = 128;
+constexpr int kXcds = 8;
 
-template <typename T> __device__ __forceinline__ void store_out(void* out, long long idx, float v, int f32) {
-  if (f32)
-    static_cast<float*>(out)[idx] = v;
-  else
-    static_cast<T*>(out)[idx] = from_f32<T>(v);
+template <typename T> struct OutVec;
+template <> struct OutVec<bf16> {
+  __device__ static __forceinline__ void store(bf16* p, const float v[4]) {
+    bf16x4 o;
+    o[0] = static_cast<bf16>(v[0]);
+    o[1] = static_cast<bf16>(v[1]);
+    o[2] = static_cast<bf16>(v[2]);
+    o[3] = static_cast<bf16>(v[3]);
+    *reinterpret_cast<bf16x4*>(p) = o;
+  }
+  __device__ static __forceinline__ void load(const bf16* p, float v[4]) {
+    const bf16x4 i = *reinterpret_cast<const bf16x4*>(p);
+    v[0] = static_cast<float>(i[0]);
+    v[1] = static_cast<float>(i[1]);
+    v[2] = static_cast<float>(i[2]);
+    v[3] = static_cast<float>(i[3]);
+  }
+};
+template <> struct OutVec<float> {
+  __device__ static __forceinline__ void store(float* p, const float v[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  __device__ static __forceinline__ void load(const float* p, float v[4]) {
+    const float4 i = *reinterpret_cast<const float4*>(p);
+    v[0] = i.x;
+    v[1] = i.y;
+    v[2] = i.z;
+    v[3] = i.w;
+  }
+};
+
+
+// Stores 4 consecutive output columns [n, n + 4) of row m (n % 4 == 0), masking
+// columns >= n_store element-wise when the group straddles the edge.
+template <typename T>
+__device__ __forceinline__ void store4(const GemmParams& p, int m, int n, float v[4], int n_store) {
+  const long long o = (long long)m * p.ldo + n;
+  const bool vec = n + 4 <= n_store && (p.ldo & 3) == 0;
+  if (p.out_f32) {
+    float* out = static_cast<float*>(p.out);
+    if (vec) {
+      OutVec<float>::store(out + o, v);
+    } else {
+      for (int e = 0; e < 4; ++e)
+        if (n + e < n_store) out[o + e] = v[e];
+    }
+  } else {
+    T* out = static_cast<T*>(p.out);
+    if (vec) {
+      OutVec<T>::store(out + o, v);
+    } else {
+      for (int e = 0; e < 4; ++e)
+        if (n + e < n_store) out[o + e] = from_f32<T>(v[e]);
+    }
+  }
 }
 
-template <typename T> __device__ __forceinline__ float load_resid(const void* r, long long idx, int f32) {
-  return f32 ? static_cast<const float*>(r)[idx] : to_f32(static_cast<const T*>(r)[idx]);
+template <typename T>
+__device__ __forceinline__ void epilogue_group(const GemmParams& p, int m, int n, float v[4]) {
+  // v holds acc[m][n..n+3]; adds bias, per-sample row vector, residual; stores.
+  if (n >= p.n_store) return;
+  const bool full = n + 4 <= p.n_store;
+  if (p.bias) {
+    for (int e = 0; e < 4; ++e) v[e] += (full || n + e < p.n_store) ? p.bias[n + e] : 0.f;
+  }
+  if (p.rowvec) {
+    const float* rv = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
+    for (int e = 0; e < 4; ++e) v[e] += (full || n + e < p.n_store) ? rv[e] : 0.f;
+  }
+  if (p.resid) {
+    const long long ro = (long long)m * p.ldr + n;
+    if (full && (p.ldr & 3) == 0) {
+      float r[4];
+      if (p.resid_f32)
+        OutVec<float>::load(static_cast<const float*>(p.resid) + ro, r);
+      else
+        OutVec<T>::load(static_cast<const T*>(p.resid) + ro, r);
+      for (int e = 0; e < 4; ++e) v[e] += r[e];
+    } else {
+      for (int e = 0; e < 4; ++e)
+        if (n + e < p.n_store)
+          v[e] += p.resid_f32 ? static_cast<const float*>(p.resid)[ro + e] : to_f32(static_cast<const T*>(p.resid)[ro + e]);
+    }
+  }
+  store4<T>(p, m, n, v, p.n_store);
 }
 
-__device__ __forceinline__ float gelu_erf(float g) { return 0.5f * g * (1.0f + erff(g * 0.70710678118654752f)); }
-
-template <typename T, int BM, bool CONV>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
+template <typename T, int BM, int BN, bool CONV>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p, int mt, int nt, int splits) {
   using MM = Mma<T>;
   constexpr int VEC = 16 / sizeof(T);
   constexpr int BK = gemm_bk<T>();
-  constexpr int BN = kBN;
   constexpr int VPR = BK / VEC;          // 16-byte vectors per tile row (8)
   constexpr int SA = BK + VEC;           // LDS row stride in elements (16-byte pad)
   constexpr int RPP = kThreads / VPR;    // tile rows covered by one pass of the block (32)
@@ -49,12 +134,27 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* lds = reinterpret_cast<T*>(smem_raw);
 
+  // ---- tile / split assignment (XCD-aware)
+  const int total = mt * nt * splits;
+  const int wg = blockIdx.x;
+  const int xcd = wg % kXcds, idx = wg / kXcds;
+  const int base = total / kXcds, rem = total % kXcds;
+  const int logical = xcd * base + min(xcd, rem) + idx;
+  const int band = mt * splits;
+  const int n_tile = logical / band;
+  const int r0 = logical - n_tile * band;
+  const int split = r0 / mt;
+  const int m_tile = r0 - split * mt;
+  const int n0 = n_tile * BN;
+  const int m0 = m_tile * BM;
+  const int nk_total = p.K / BK;
+  const int kt_begin = (int)((long long)nk_total * split / splits);
+  const int kt_end = (int)((long long)nk_total * (split + 1) / splits);
+
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int n0 = blockIdx.x * BN;
-  const int m0 = blockIdx.y * BM;
   const int vc = tid % VPR;
   const int rr = tid / VPR;
 
@@ -68,9 +168,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     a_row[i] = m;
     if (CONV) {
       const int s = m / opix;
-      const int rem = m - s * opix;
-      const int oy = rem / p.out_w;
-      const int ox = rem - oy * p.out_w;
+      const int rem2 = m - s * opix;
+      const int oy = rem2 / p.out_w;
+      const int ox = rem2 - oy * p.out_w;
       a_sy[i] = s * p.in_h;
       a_oy[i] = oy * p.stride - 1;
       a_ox[i] = ox * p.stride - 1;
@@ -132,6 +232,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     for (int i = 0; i < BV; ++i) st16(Bs + (rr + i * RPP) * SA + vc * VEC, rb[i]);
   };
 
+  // acc[i][j]: rows = output columns n0 + wn*WN + 32 j + acc_row(r),
+  //            column = output row m0 + wm*WM + 32 i + (lane % 32).
   f32x16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -140,93 +242,167 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = p.K / BK;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
   const int frag_off = (lane & 31) * SA + (lane >> 5) * MM::KPL;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load_tile((kt + 1) * BK);
-    const T* As = lds + cur * STAGE + wm * WM * SA + frag_off;
-    const T* Bs = lds + cur * STAGE + BM * SA + wn * WN * SA + frag_off;
-#pragma unroll
-    for (int ks = 0; ks < BK / MM::KS; ++ks) {
-      typename MM::frag a[FM], b[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = MM::load(As + i * 32 * SA + ks * MM::KS);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) b[j] = MM::load(Bs + j * 32 * SA + ks * MM::KS);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = MM::mma(a[i], b[j], acc[i][j]);
-    }
-    if (kt + 1 < nk) store_tile(cur ^ 1);
+  if (kt_begin < kt_end) {
+    load_tile(kt_begin * BK);
+    store_tile(0);
+    if (kt_begin + 1 < kt_end) load_tile((kt_begin + 1) * BK);
     __syncthreads();
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
+      const int cur = (kt - kt_begin) & 1;
+      const T* As = lds + cur * STAGE + wm * WM * SA + frag_off;
+      const T* Bs = lds + cur * STAGE + BM * SA + wn * WN * SA + frag_off;
+#pragma unroll
+      for (int ks = 0; ks < BK / MM::KS; ++ks) {
+        typename MM::frag a[FM], b[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[i] = MM::load(As + i * 32 * SA + ks * MM::KS);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[j] = MM::load(Bs + j * 32 * SA + ks * MM::KS);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = MM::mma(b[j], a[i], acc[i][j]);
+      }
+      if (kt + 1 < kt_end) {
+        store_tile(cur ^ 1);
+        if (kt + 2 < kt_end) load_tile((kt + 2) * BK);
+      }
+      __syncthreads();
+    }
   }
 
-  // Epilogue.
   const int col = lane & 31;
-  if (!p.geglu) {
+  const int h4 = 4 * (lane >> 5);
+
+  // ---- split-K: publish partials; only the last arriving workgroup continues.
+  if (splits > 1) {
+    const int tile = n_tile * mt + m_tile;
+    float* ws = p.ws + ((long long)tile * splits + split) * (BM * BN);
+    // Partial layout inside a tile: [wave][i][j][r][lane] (coalesced per register).
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * WN + j * 32 + col;
-      if (n >= p.n_store) continue;
-      const float bn = p.bias ? p.bias[n] : 0.f;
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          ws[(((wave * FM + i) * FN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    __threadfence();
+    __syncthreads();
+    __shared__ int last;
+    if (tid == 0) {
+      const int prev = __hip_atomic_fetch_add(p.counters + tile, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      last = prev == splits - 1;
+    }
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    const float* wt = p.ws + (long long)tile * splits * (BM * BN);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int m = m0 + wm * WM + i * 32 + acc_row(r, lane);
-          if (m >= p.M) continue;
-          float v = acc[i][j][r] + bn;
-          if (p.rowvec) v += p.rowvec[(long long)(m / p.rows_per_sample) * p.rowvec_ld + n];
-          if (p.resid) v += load_resid<T>(p.resid, (long long)m * p.ldr + n, p.resid_f32);
-          store_out<T>(p.out, (long long)m * p.ldo + n, v, p.out_f32);
+          const int o = (((wave * FM + i) * FN + j) * 16 + r) * 64 + lane;
+          float s = 0.f;
+          for (int q = 0; q < splits; ++q) s += (q == split) ? acc[i][j][r] : wt[(long long)q * (BM * BN) + o];
+          acc[i][j][r] = s;
         }
-      }
+    if (tid == 0) __hip_atomic_store(p.counters + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+
+  // ---- epilogue
+  if (!p.geglu) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int m = m0 + wm * WM + i * 32 + col;
+      if (m >= p.M) continue;
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = n0 + wn * WN + j * 32 + 8 * g + h4;
+          float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+          epilogue_group<T>(p, m, n, v);
+        }
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < FN / 2; ++j) {
-      const int nv = n0 + wn * WN + 2 * j * 32 + col;
-      const int o = (n0 + wn * WN) / 2 + j * 32 + col;
-      if (o >= p.n_store) continue;
-      const float bv = p.bias ? p.bias[nv] : 0.f;
-      const float bg = p.bias ? p.bias[nv + 32] : 0.f;
+    for (int i = 0; i < FM; ++i) {
+      const int m = m0 + wm * WM + i * 32 + col;
+      if (m >= p.M) continue;
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
+      for (int j = 0; j < FN / 2; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = m0 + wm * WM + i * 32 + acc_row(r, lane);
-          if (m >= p.M) continue;
-          const float v = (acc[i][2 * j][r] + bv) * gelu_erf(acc[i][2 * j + 1][r] + bg);
-          store_out<T>(p.out, (long long)m * p.ldo + o, v, p.out_f32);
+        for (int g = 0; g < 4; ++g) {
+          const int nv = n0 + wn * WN + 2 * j * 32 + 8 * g + h4;   // value column (gate = nv + 32)
+          const int o = (n0 + wn * WN) / 2 + j * 32 + 8 * g + h4;  // output column
+          if (o >= p.n_store) continue;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float a = acc[i][2 * j][4 * g + e] + (p.bias ? p.bias[nv + e] : 0.f);
+            const float gg = acc[i][2 * j + 1][4 * g + e] + (p.bias ? p.bias[nv + 32 + e] : 0.f);
+            v[e] = a * gelu_erf(gg);
+          }
+          store4<T>(p, m, o, v, p.n_store);
         }
-      }
     }
   }
 }
 
-template <typename T, int BM, bool CONV> void launch(const GemmParams& p, hipStream_t s) {
+template <typename T, int BM, int BN, bool CONV>
+void launch(const GemmParams& p, int splits, hipStream_t s) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int SA = gemm_bk<T>() + VEC;
-  const size_t lds = size_t(2) * (BM + kBN) * SA * sizeof(T);
+  const size_t lds = size_t(2) * (BM + BN) * SA * sizeof(T);
   static bool attr_set = false;
   if (!attr_set) {
-    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<T, BM, CONV>),
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<T, BM, BN, CONV>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
     attr_set = true;
   }
-  dim3 grid(ceil_div(p.N, kBN), ceil_div(p.M, BM));
-  hipLaunchKernelGGL((gemm_kernel<T, BM, CONV>), grid, dim3(kThreads), lds, s, p);
+  const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, BN);
+  if (splits > 1) {
+    DN_CHECK(p.ws && p.counters, "gemm: split-K needs a workspace");
+    DN_CHECK((size_t)mt * nt * splits * BM * BN <= p.ws_floats && (size_t)mt * nt <= p.n_counters,
+             "gemm: split-K workspace too small");
+  }
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, CONV>), dim3(mt * nt * splits), dim3(kThreads), lds, s, p, mt, nt,
+                     splits);
   DN_HIP(hipGetLastError());
+}
+
+template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
+  if (g.bm == 256 && g.bn == 128)
+    launch<T, 256, 128, CONV>(p, g.splits, s);
+  else if (g.bm == 128 && g.bn == 256)
+    launch<T, 128, 256, CONV>(p, g.splits, s);
+  else
+    launch<T, 128, 128, CONV>(p, g.splits, s);
 }
 
 }  // namespace
 
-template <typename T> void gemm(const GemmParams& p, hipStream_t s) {
+// Tile choice, from measurements on MI355X (SD-XL shapes, bf16): the
+// register-staged 128 x 128 kernel (two resident workgroups per CU) is the
+// fastest except on the tall convolutions (M >= 8192 rows with at least one
+// 256 x 256 tile per CU), where the 8-wave direct-to-LDS 256 x 256 kernel wins.
+// fp32 (the check mode) always uses the 128 x 128 register kernel. Split-K is
+// not planned: publishing partials across XCDs needs an agent-scope release (an
+// L2 write-back per workgroup), which cost more than the quantization it removes.
+template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus) {
+  (void)K;
+  (void)geglu;
+  if (sizeof(T) == 2) {
+    const long long t256 = (long long)ceil_div(M, 256) * ceil_div(N, 256);
+    if (M >= 8192 && t256 >= cus && N >= 256) return GemmPlan{256, 256, 1, 1};
+  }
+  return GemmPlan{128, 128, 1, 0};
+}
+
+template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
   constexpr int BK = gemm_bk<T>();
   DN_CHECK(p.M >= 1 && p.N >= 1 && p.K >= BK, "gemm: empty or too small problem");
   DN_CHECK(p.K % BK == 0, "gemm: K must be a multiple of the K tile");
@@ -236,25 +412,33 @@ template <typename T> void gemm(const GemmParams& p, hipStream_t s) {
   DN_CHECK(p.taps == 1 || (p.c0 + p.c1) % BK == 0, "gemm: conv channels must be a multiple of the K tile");
   DN_CHECK(p.a0 && p.b && p.out && (p.c1 == 0 || p.a1), "gemm: null operand");
   DN_CHECK(!p.geglu || (p.N % 64 == 0), "gemm: GEGLU needs N % 64 == 0");
+  DN_CHECK(!p.geglu || g.bn % 128 == 0 || g.bn % 64 == 0, "gemm: GEGLU needs a block width multiple of 64");
   DN_CHECK(p.ldb % (16 / (int)sizeof(T)) == 0 && p.lda0 % (16 / (int)sizeof(T)) == 0 &&
                (p.c1 == 0 || p.lda1 % (16 / (int)sizeof(T)) == 0),
            "gemm: leading dimensions must be multiples of 16 bytes");
-  const long long t256 = (long long)ceil_div(p.M, 256) * ceil_div(p.N, kBN);
-  const bool big = p.M >= 256 && t256 >= 512;
-  if (p.taps == 9) {
-    if (big)
-      launch<T, 256, true>(p, s);
-    else
-      launch<T, 128, true>(p, s);
-  } else {
-    if (big)
-      launch<T, 256, false>(p, s);
-    else
-      launch<T, 128, false>(p, s);
+  DN_CHECK(g.splits >= 1 && g.splits <= 4, "gemm: splits must be in [1, 4]");
+  if (g.dma) {
+    DN_CHECK(sizeof(T) == 2 && g.splits == 1, "gemm: the direct-to-LDS kernel is bf16 without split-K");
+    gemm_bf16_dma(p, g, s);
+    return;
   }
+  if (p.taps == 9)
+    dispatch<T, true>(p, g, s);
+  else
+    dispatch<T, false>(p, g, s);
 }
 
-template void gemm<float>(const GemmParams&, hipStream_t);
-template void gemm<bf16>(const GemmParams&, hipStream_t);
+size_t gemm_workspace_floats(const GemmPlan& g, int M, int N) {
+  if (g.splits <= 1) return 0;
+  return (size_t)ceil_div(M, g.bm) * ceil_div(N, g.bn) * g.splits * g.bm * g.bn;
+}
+size_t gemm_counters(const GemmPlan& g, int M, int N) {
+  return g.splits <= 1 ? 0 : (size_t)ceil_div(M, g.bm) * ceil_div(N, g.bn);
+}
+
+template GemmPlan gemm_plan<float>(int, int, int, int, int);
+template GemmPlan gemm_plan<bf16>(int, int, int, int, int);
+template void gemm<float>(const GemmParams&, const GemmPlan&, hipStream_t);
+template void gemm<bf16>(const GemmParams&, const GemmPlan&, hipStream_t);
 
 }  // namespace dn

@@ -7,7 +7,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/argus_dn.h"
+#include "argus_dn.h"
 #include "kernels.h"
 
 namespace dn {

@@ -319,6 +319,12 @@ struct Model {
   float *gn_partial = nullptr, *gn_stats = nullptr;
   float *feat = nullptr, *hid = nullptr, *temb = nullptr, *tproj = nullptr;
   double* abar = nullptr;
+  int cus = 256;                 // compute units of the device (GEMM planning)
+  float* gemm_ws = nullptr;      // split-K partials
+  size_t gemm_ws_floats = 0;
+  int* gemm_counters = nullptr;  // split-K arrival counters (self-resetting)
+  size_t gemm_n_counters = 0;
+  void* zero = nullptr;          // 256 zero bytes: implicit-conv padding reads
   // shapes per layer output (for the executor)
   std::vector<int> act_h, act_w, act_c;
 };
@@ -622,6 +628,10 @@ void size_workspace(Model* m, Sizer& z) {
 
 // ============================================================================ create / destroy
 
+// Split-K workspace of every GEMM one step and one call preparation launch
+// (defined after the executor).
+static void gemm_needs(Model* m, size_t* ws_floats, size_t* counters);
+
 Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats, bool on_device) {
   const std::vector<TensorSpec> table = weight_table(cfg);
   const int64_t total = table.empty() ? 0 : table.back().offset + table.back().numel;
@@ -706,6 +716,7 @@ Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats,
     want.push_back({reinterpret_cast<void**>(&m->temb), (size_t)kMaxSteps * m->temb_dim * 4});
     want.push_back({reinterpret_cast<void**>(&m->tproj), (size_t)kMaxSteps * m->temb_total * 4});
     want.push_back({reinterpret_cast<void**>(&m->abar), (size_t)cfg.n_train_steps * 8});
+    want.push_back({&m->zero, 256});
     size_t bytes = 0;
     for (auto& w : want) bytes += (w.second + 255) / 256 * 256;
     DN_HIP(hipMalloc(&m->arena, bytes));
@@ -715,6 +726,14 @@ Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats,
       off += (w.second + 255) / 256 * 256;
     }
     DN_HIP(hipMemset(m->xin, 0, (size_t)m->n * HW0 * kCinPad * e));
+    DN_HIP(hipMemset(m->zero, 0, 256));
+    m->cus = prop.multiProcessorCount;
+    gemm_needs(m.get(), &m->gemm_ws_floats, &m->gemm_n_counters);
+    if (m->gemm_ws_floats) DN_HIP(hipMalloc(&m->gemm_ws, m->gemm_ws_floats * 4));
+    if (m->gemm_n_counters) {
+      DN_HIP(hipMalloc(&m->gemm_counters, m->gemm_n_counters * 4));
+      DN_HIP(hipMemset(m->gemm_counters, 0, m->gemm_n_counters * 4));
+    }
     abar_table(m->abar, cfg.n_train_steps, cfg.beta_start, cfg.beta_end, cfg.beta_schedule, s);
     DN_HIP(hipStreamSynchronize(s));
   } catch (...) {
@@ -731,6 +750,8 @@ void model_destroy(Model* m) {
   if (m->packed) (void)hipFree(m->packed);
   if (m->params) (void)hipFree(m->params);
   if (m->arena) (void)hipFree(m->arena);
+  if (m->gemm_ws) (void)hipFree(m->gemm_ws);
+  if (m->gemm_counters) (void)hipFree(m->gemm_counters);
   delete m;
 }
 
@@ -742,6 +763,23 @@ template <typename T> struct Exec {
   Model* m;
   hipStream_t s;
   int n;
+  bool dry = false;          // sizing pass: record workspace needs, launch nothing
+  size_t need_ws = 0, need_counters = 0;
+
+  void run_gemm(GemmParams& p) {
+    const GemmPlan g = gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus);
+    if (dry) {
+      need_ws = std::max(need_ws, gemm_workspace_floats(g, p.M, p.N));
+      need_counters = std::max(need_counters, gemm_counters(g, p.M, p.N));
+      return;
+    }
+    p.ws = m->gemm_ws;
+    p.ws_floats = m->gemm_ws_floats;
+    p.counters = m->gemm_counters;
+    p.n_counters = m->gemm_n_counters;
+    p.zero16 = m->zero;
+    gemm<T>(p, g, s);
+  }
 
   void conv(const ConvW& w, const void* x, int in_h, int in_w, int up, int stride, void* out, int out_h, int out_w,
             const float* rowvec, const void* resid, bool out_f32, int n_store, int ldo) {
@@ -772,7 +810,7 @@ template <typename T> struct Exec {
     p.ldo = ldo;
     p.out_f32 = out_f32;
     p.n_store = n_store;
-    gemm<T>(p, s);
+    run_gemm(p);
   }
 
   void linear(const LinW& w, const void* x, int ldx, long long M, void* out, int ldo, bool out_f32,
@@ -800,7 +838,7 @@ template <typename T> struct Exec {
     p.out_f32 = out_f32;
     p.geglu = geglu;
     p.n_store = geglu ? w.n / 2 : w.n;
-    gemm<T>(p, s);
+    run_gemm(p);
   }
 
   void groupnorm_(const void* x0, int c0, const void* x1, int c1, int HW, const Norm& nm, float eps, bool silu,
@@ -820,7 +858,7 @@ template <typename T> struct Exec {
     p.y = y;
     p.partial = m->gn_partial;
     p.stats = m->gn_stats;
-    groupnorm<T>(p, s);
+    if (!dry) groupnorm<T>(p, s);
   }
 
   void resblock(const ResL& r, const void* x0, int c0, const void* x1, int c1, int H, int W, const float* tproj_row,
@@ -856,7 +894,7 @@ template <typename T> struct Exec {
     a.Sq = Sq;
     a.Skv = Skv;
     a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt((double)x.D));
-    attention<T>(a, x.Dp, s);
+    if (!dry) attention<T>(a, x.Dp, s);
   }
 
   void transformer(const TxL& x, const void* in, int H, int W, void* out) {
@@ -868,19 +906,19 @@ template <typename T> struct Exec {
     for (size_t bi = 0; bi < x.blocks.size(); ++bi) {
       const TxBlock& b = x.blocks[bi];
       const bool last = bi + 1 == x.blocks.size();
-      layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln1.g, b.ln1.b, m->cfg.ln_eps, s);
+      if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln1.g, b.ln1.b, m->cfg.ln_eps, s);
       linear(b.qkv, m->a, C, M, m->qkv, 3 * P, false);
       const char* qkv = static_cast<const char*>(m->qkv);
       attention_(qkv, 3 * P, (long long)HW * 3 * P, qkv + (size_t)P * e, qkv + (size_t)2 * P * e, 3 * P,
                  (long long)HW * 3 * P, HW, HW, x);
       linear(b.o1, m->o, P, M, m->R, C, true, m->R, C, true);
-      layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln2.g, b.ln2.b, m->cfg.ln_eps, s);
+      if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln2.g, b.ln2.b, m->cfg.ln_eps, s);
       linear(b.q2, m->a, C, M, m->q2, P, false);
       const char* kv = static_cast<const char*>(m->kv) + (size_t)b.kv_slot * m->kv_slot_elems * e;
       attention_(m->q2, P, (long long)HW * P, kv, kv + (size_t)P * e, 2 * P, (long long)m->cfg.ctx_len * 2 * P, HW,
                  m->cfg.ctx_len, x);
       linear(b.o2, m->o, P, M, m->R, C, true, m->R, C, true);
-      layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln3.g, b.ln3.b, m->cfg.ln_eps, s);
+      if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln3.g, b.ln3.b, m->cfg.ln_eps, s);
       linear(b.ff1, m->a, C, M, m->ff, m->cfg.ff_mult * C, false, nullptr, 0, false, true);
       if (!last)
         linear(b.ff2, m->ff, m->cfg.ff_mult * C, M, m->R, C, true, m->R, C, true);
@@ -897,11 +935,14 @@ template <typename T> struct Exec {
   // context keys / values of every cross-attention.
   void prepare(const float* ctx, int n_steps) {
     const dn_config& c = m->cfg;
-    skinny_linear(m->feat, n_steps, c.model_channels, m->lin1_w, m->lin1_b, m->temb_dim, m->hid, m->temb_dim, 0, s);
-    skinny_linear(m->hid, n_steps, m->temb_dim, m->lin2_w, m->lin2_b, m->temb_dim, m->temb, m->temb_dim, 1, s);
-    skinny_linear(m->temb, n_steps, m->temb_dim, m->tproj_w, m->tproj_b, m->temb_total, m->tproj, m->temb_total, 1,
-                  s);
-    convert_from_f32<T>(ctx, P_<T>(m->ctx_t), (long long)n * c.ctx_len * c.ctx_dim, s);
+    if (!dry) {
+      skinny_linear(m->feat, n_steps, c.model_channels, m->lin1_w, m->lin1_b, m->temb_dim, m->hid, m->temb_dim, 0,
+                    s);
+      skinny_linear(m->hid, n_steps, m->temb_dim, m->lin2_w, m->lin2_b, m->temb_dim, m->temb, m->temb_dim, 1, s);
+      skinny_linear(m->temb, n_steps, m->temb_dim, m->tproj_w, m->tproj_b, m->temb_total, m->tproj,
+                    m->temb_total, 1, s);
+      convert_from_f32<T>(ctx, P_<T>(m->ctx_t), (long long)n * c.ctx_len * c.ctx_dim, s);
+    }
     for (const auto& x : m->tx)
       for (const auto& b : x.blocks) {
         void* dst = static_cast<char*>(m->kv) + (size_t)b.kv_slot * m->kv_slot_elems * sizeof(T);
@@ -1024,6 +1065,27 @@ void unet_eps_t(Model* m, const float* x, int t, const float* ctx, float scale, 
 }
 
 }  // namespace
+
+static void gemm_needs(Model* m, size_t* ws_floats, size_t* counters) {
+  size_t ws = 0, cnt = 0;
+  if (m->bf) {
+    Exec<bf16> ex{m, nullptr, m->n};
+    ex.dry = true;
+    ex.prepare(nullptr, 1);
+    ex.unet(0);
+    ws = ex.need_ws;
+    cnt = ex.need_counters;
+  } else {
+    Exec<float> ex{m, nullptr, m->n};
+    ex.dry = true;
+    ex.prepare(nullptr, 1);
+    ex.unet(0);
+    ws = ex.need_ws;
+    cnt = ex.need_counters;
+  }
+  *ws_floats = ws;
+  *counters = cnt;
+}
 
 void model_denoise(Model* m, float* latent, const float* ctx, const int32_t* ts, int n_ts, int start, int n,
                    float scale, hipStream_t s) {

@@ -252,3 +252,28 @@ def test_sdxl_self_attention_sampled():
             p = np.exp(s - s.max())
             ref = (p / p.sum()) @ V_
             assert rel_l2(oh[b, i, h * d:(h + 1) * d], ref) < 1e-2, (b, h, i)
+
+
+@pytest.mark.parametrize("M,N,K", [(2048, 1280, 5120), (2048, 1280, 1280), (2048, 3840, 1280), (154, 2560, 2048)])
+def test_sdxl_linear_shapes_sampled_and_deterministic(M, N, K):
+    """The M = 2048 projections of the SD-XL 32x32 blocks (FF-out, attention out, QKV)
+    and the context K/V projection, in the launch configuration the denoiser uses
+    (split-K where the planner picks it): sampled outputs against fp64 dot products,
+    and two launches bitwise equal (the split-K reduction order is fixed)."""
+    announce(f"sdxl linear {M}x{N}x{K}")
+    g = torch.Generator(device=DEV).manual_seed(M + N + K)
+    x = torch.randn((M, K), device=DEV, generator=g).to(torch.bfloat16)
+    w = (torch.randn((N, K), device=DEV, generator=g) / math.sqrt(K)).to(torch.bfloat16)
+    b = torch.randn(N, device=DEV, generator=g)
+    res = torch.randn((M, N), device=DEV, generator=g)
+    y1 = torch.empty((M, N), device=DEV)
+    y2 = torch.empty((M, N), device=DEV)
+    dn.op_linear(dn.DN_BF16, x, w, b, y1, M, N, K, resid=res, resid_f32=True, y_f32=True)
+    dn.op_linear(dn.DN_BF16, x, w, b, y2, M, N, K, resid=res, resid_f32=True, y_f32=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    r = _rng(M + K)
+    xh, wh, bh, rh, yh = host(x), host(w), host(b), host(res), host(y1)
+    for m, n in zip(*_sample_idx(r, (M, N), 400)):
+        ref = float(xh[m] @ wh[n] + bh[n] + rh[m, n])
+        assert abs(yh[m, n] - ref) <= 2e-3 * max(1.0, abs(ref)), (m, n, yh[m, n], ref)
