@@ -51,50 +51,33 @@ void* lookup_ws(int dev) {
 
 bool is_dtype(int32_t d) { return d == DN_FP32 || d == DN_BF16; }
 
-// Per-device split-K workspace of the single-kernel GEMM entry points (grow-only;
-// growing waits for the device so that no queued launch still uses the old one).
-struct OpWs {
-  float* ws = nullptr;
-  size_t ws_floats = 0;
-  int* counters = nullptr;
-  size_t n_counters = 0;
+// Per-device state of the single-kernel GEMM entry points: CU count (tile
+// planning) and a zero block for implicit-conv padding reads.
+struct OpDev {
   int cus = 0;
-  void* zero = nullptr;  // zero block for implicit-conv padding reads
+  void* zero = nullptr;
 };
 std::mutex g_op_mu;
-std::vector<OpWs> g_op_ws;
+std::vector<OpDev> g_op_dev;
 
 template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
   int dev = 0;
   DN_HIP(hipGetDevice(&dev));
-  std::lock_guard<std::mutex> lk(g_op_mu);
-  if ((int)g_op_ws.size() <= dev) g_op_ws.resize(dev + 1);
-  OpWs& w = g_op_ws[dev];
-  if (!w.cus) {
-    hipDeviceProp_t prop;
-    DN_HIP(hipGetDeviceProperties(&prop, dev));
-    w.cus = prop.multiProcessorCount;
-    DN_HIP(hipMalloc(&w.zero, 256));
-    DN_HIP(hipMemset(w.zero, 0, 256));
+  OpDev w;
+  {
+    std::lock_guard<std::mutex> lk(g_op_mu);
+    if ((int)g_op_dev.size() <= dev) g_op_dev.resize(dev + 1);
+    OpDev& d = g_op_dev[dev];
+    if (!d.cus) {
+      hipDeviceProp_t prop;
+      DN_HIP(hipGetDeviceProperties(&prop, dev));
+      DN_HIP(hipMalloc(&d.zero, 256));
+      DN_HIP(hipMemset(d.zero, 0, 256));
+      d.cus = prop.multiProcessorCount;
+    }
+    w = d;
   }
   const dn::GemmPlan g = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, w.cus);
-  const size_t need = dn::gemm_workspace_floats(g, p.M, p.N), nc = dn::gemm_counters(g, p.M, p.N);
-  if (need > w.ws_floats || nc > w.n_counters) {
-    DN_HIP(hipDeviceSynchronize());
-    if (w.ws) DN_HIP(hipFree(w.ws));
-    if (w.counters) DN_HIP(hipFree(w.counters));
-    w.ws = nullptr;
-    w.counters = nullptr;
-    w.ws_floats = std::max(need, w.ws_floats);
-    w.n_counters = std::max(nc, w.n_counters);
-    DN_HIP(hipMalloc(&w.ws, w.ws_floats * 4 + 4));
-    DN_HIP(hipMalloc(&w.counters, w.n_counters * 4 + 4));
-    DN_HIP(hipMemset(w.counters, 0, w.n_counters * 4 + 4));
-  }
-  p.ws = w.ws;
-  p.ws_floats = w.ws_floats;
-  p.counters = w.counters;
-  p.n_counters = w.n_counters;
   p.zero16 = w.zero;
   dn::gemm<T>(p, g, s);
 }

@@ -7,7 +7,7 @@
 // (fused QKV, attention outputs, GEGLU feed-forward, projections).
 //
 // Tiling: 256 threads = 4 waves in a 2x2 grid; block tile BM x BN in
-// {256x128, 128x256, 128x128}, wave tile (BM/2) x (BN/2) built from 32x32x16 MFMA blocks; K
+// {128x128, 64x128, 64x64, 256x128, 128x256}, wave tile (BM/2) x (BN/2) built from 32x32x16 MFMA blocks; K
 // step BK = 128 bytes of each row (64 bf16 / 32 fp32), staged through
 // double-buffered LDS (one barrier per K step; the next tile's global loads are
 // issued a full K step ahead). The MFMA is issued as C^T = B A^T so that each
@@ -18,10 +18,6 @@
 // Work distribution: tiles are numbered so that each XCD (consecutive
 // workgroup ids go round-robin over the 8 XCDs) works through a contiguous band
 // of output columns with all row tiles, keeping that band of B in its L2.
-// Optional split-K: each of S workgroups of a tile reduces a K range into fp32
-// partials; the last one to arrive (integer atomic counter per tile) sums the S
-// partials in split order and runs the epilogue, so the result does not depend
-// on arrival order. The counter is reset by that workgroup.
 #include "kernels.h"
 
 namespace dn {
@@ -118,7 +114,7 @@ __device__ __forceinline__ void epilogue_group(const GemmParams& p, int m, int n
 }
 
 template <typename T, int BM, int BN, bool CONV>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p, int mt, int nt, int splits) {
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p, int mt, int nt) {
   using MM = Mma<T>;
   constexpr int VEC = 16 / sizeof(T);
   constexpr int BK = gemm_bk<T>();
@@ -134,22 +130,18 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p, int mt, in
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* lds = reinterpret_cast<T*>(smem_raw);
 
-  // ---- tile / split assignment (XCD-aware)
-  const int total = mt * nt * splits;
+  // ---- tile assignment (XCD-aware: each XCD walks a contiguous band of columns)
+  const int total = mt * nt;
   const int wg = blockIdx.x;
   const int xcd = wg % kXcds, idx = wg / kXcds;
   const int base = total / kXcds, rem = total % kXcds;
   const int logical = xcd * base + min(xcd, rem) + idx;
-  const int band = mt * splits;
-  const int n_tile = logical / band;
-  const int r0 = logical - n_tile * band;
-  const int split = r0 / mt;
-  const int m_tile = r0 - split * mt;
+  const int n_tile = logical / mt;
+  const int m_tile = logical - n_tile * mt;
   const int n0 = n_tile * BN;
   const int m0 = m_tile * BM;
-  const int nk_total = p.K / BK;
-  const int kt_begin = (int)((long long)nk_total * split / splits);
-  const int kt_end = (int)((long long)nk_total * (split + 1) / splits);
+  const int kt_begin = 0;
+  const int kt_end = p.K / BK;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -275,43 +267,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p, int mt, in
   const int col = lane & 31;
   const int h4 = 4 * (lane >> 5);
 
-  // ---- split-K: publish partials; only the last arriving workgroup continues.
-  if (splits > 1) {
-    const int tile = n_tile * mt + m_tile;
-    float* ws = p.ws + ((long long)tile * splits + split) * (BM * BN);
-    // Partial layout inside a tile: [wave][i][j][r][lane] (coalesced per register).
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          ws[(((wave * FM + i) * FN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
-    __threadfence();
-    __syncthreads();
-    __shared__ int last;
-    if (tid == 0) {
-      const int prev = __hip_atomic_fetch_add(p.counters + tile, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      last = prev == splits - 1;
-    }
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
-    const float* wt = p.ws + (long long)tile * splits * (BM * BN);
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int o = (((wave * FM + i) * FN + j) * 16 + r) * 64 + lane;
-          float s = 0.f;
-          for (int q = 0; q < splits; ++q) s += (q == split) ? acc[i][j][r] : wt[(long long)q * (BM * BN) + o];
-          acc[i][j][r] = s;
-        }
-    if (tid == 0) __hip_atomic_store(p.counters + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-
   // ---- epilogue
   if (!p.geglu) {
 #pragma unroll
@@ -353,7 +308,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p, int mt, in
 }
 
 template <typename T, int BM, int BN, bool CONV>
-void launch(const GemmParams& p, int splits, hipStream_t s) {
+void launch(const GemmParams& p, hipStream_t s) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int SA = gemm_bk<T>() + VEC;
   const size_t lds = size_t(2) * (BM + BN) * SA * sizeof(T);
@@ -364,42 +319,42 @@ void launch(const GemmParams& p, int splits, hipStream_t s) {
     attr_set = true;
   }
   const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, BN);
-  if (splits > 1) {
-    DN_CHECK(p.ws && p.counters, "gemm: split-K needs a workspace");
-    DN_CHECK((size_t)mt * nt * splits * BM * BN <= p.ws_floats && (size_t)mt * nt <= p.n_counters,
-             "gemm: split-K workspace too small");
-  }
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, CONV>), dim3(mt * nt * splits), dim3(kThreads), lds, s, p, mt, nt,
-                     splits);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, CONV>), dim3(mt * nt), dim3(kThreads), lds, s, p, mt, nt);
   DN_HIP(hipGetLastError());
 }
 
 template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
   if (g.bm == 256 && g.bn == 128)
-    launch<T, 256, 128, CONV>(p, g.splits, s);
+    launch<T, 256, 128, CONV>(p, s);
   else if (g.bm == 128 && g.bn == 256)
-    launch<T, 128, 256, CONV>(p, g.splits, s);
+    launch<T, 128, 256, CONV>(p, s);
+  else if (g.bm == 64 && g.bn == 128)
+    launch<T, 64, 128, CONV>(p, s);
+  else if (g.bm == 64 && g.bn == 64)
+    launch<T, 64, 64, CONV>(p, s);
   else
-    launch<T, 128, 128, CONV>(p, g.splits, s);
+    launch<T, 128, 128, CONV>(p, s);
 }
 
 }  // namespace
 
-// Tile choice, from measurements on MI355X (SD-XL shapes, bf16): the
-// register-staged 128 x 128 kernel (two resident workgroups per CU) is the
-// fastest except on the tall convolutions (M >= 8192 rows with at least one
-// 256 x 256 tile per CU), where the 8-wave direct-to-LDS 256 x 256 kernel wins.
-// fp32 (the check mode) always uses the 128 x 128 register kernel. Split-K is
-// not planned: publishing partials across XCDs needs an agent-scope release (an
-// L2 write-back per workgroup), which cost more than the quantization it removes.
+// Tile choice, from measurements on MI355X (SD-XL shapes, bf16):
+//  - tall convolutions (M >= 8192 rows, at least one 256 x 256 tile per CU):
+//    the 8-wave direct-to-LDS 256 x 256 kernel;
+//  - problems with fewer 128 x 128 tiles than CUs (the M = 2048, N = 1280
+//    projections): 64 x 64 tiles, so that every CU gets work (GEGLU needs
+//    64-column value/gate pairs per wave, i.e. a block width of 128 or 256);
+//  - otherwise the register-staged 128 x 128 kernel (two resident workgroups per CU).
+// fp32 (the check mode) takes the same register-kernel shapes.
 template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus) {
   (void)K;
-  (void)geglu;
   if (sizeof(T) == 2) {
     const long long t256 = (long long)ceil_div(M, 256) * ceil_div(N, 256);
-    if (M >= 8192 && t256 >= cus && N >= 256) return GemmPlan{256, 256, 1, 1};
+    if (M >= 8192 && t256 >= cus && N >= 256) return GemmPlan{256, 256, 1};
   }
-  return GemmPlan{128, 128, 1, 0};
+  const long long t128 = (long long)ceil_div(M, 128) * ceil_div(N, 128);
+  if (!geglu && t128 < cus) return GemmPlan{64, 64, 0};
+  return GemmPlan{128, 128, 0};
 }
 
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
@@ -412,13 +367,12 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
   DN_CHECK(p.taps == 1 || (p.c0 + p.c1) % BK == 0, "gemm: conv channels must be a multiple of the K tile");
   DN_CHECK(p.a0 && p.b && p.out && (p.c1 == 0 || p.a1), "gemm: null operand");
   DN_CHECK(!p.geglu || (p.N % 64 == 0), "gemm: GEGLU needs N % 64 == 0");
-  DN_CHECK(!p.geglu || g.bn % 128 == 0 || g.bn % 64 == 0, "gemm: GEGLU needs a block width multiple of 64");
+  DN_CHECK(!p.geglu || (g.bn / 2) % 64 == 0, "gemm: GEGLU needs 64-column value/gate pairs per wave");
   DN_CHECK(p.ldb % (16 / (int)sizeof(T)) == 0 && p.lda0 % (16 / (int)sizeof(T)) == 0 &&
                (p.c1 == 0 || p.lda1 % (16 / (int)sizeof(T)) == 0),
            "gemm: leading dimensions must be multiples of 16 bytes");
-  DN_CHECK(g.splits >= 1 && g.splits <= 4, "gemm: splits must be in [1, 4]");
   if (g.dma) {
-    DN_CHECK(sizeof(T) == 2 && g.splits == 1, "gemm: the direct-to-LDS kernel is bf16 without split-K");
+    DN_CHECK(sizeof(T) == 2, "gemm: the direct-to-LDS kernel is bf16 only");
     gemm_bf16_dma(p, g, s);
     return;
   }
@@ -426,14 +380,6 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
     dispatch<T, true>(p, g, s);
   else
     dispatch<T, false>(p, g, s);
-}
-
-size_t gemm_workspace_floats(const GemmPlan& g, int M, int N) {
-  if (g.splits <= 1) return 0;
-  return (size_t)ceil_div(M, g.bm) * ceil_div(N, g.bn) * g.splits * g.bm * g.bn;
-}
-size_t gemm_counters(const GemmPlan& g, int M, int N) {
-  return g.splits <= 1 ? 0 : (size_t)ceil_div(M, g.bm) * ceil_div(N, g.bn);
 }
 
 template GemmPlan gemm_plan<float>(int, int, int, int, int);

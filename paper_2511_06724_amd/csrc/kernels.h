@@ -37,24 +37,17 @@ struct GemmParams {
   int ldo = 0, out_f32 = 0;
   int n_store = 0;  // output columns written
   int geglu = 0;
-  // split-K workspace (only read when the plan splits K)
-  float* ws = nullptr;
-  size_t ws_floats = 0;
-  int* counters = nullptr;  // one per output tile, zero between launches
-  size_t n_counters = 0;
   const void* zero16 = nullptr;  // >= 16 zero bytes (implicit-conv padding reads, direct-to-LDS path)
 };
 
-// Block tile (bm x bn) and number of K splits of one GEMM launch.
+// Block tile (bm x bn) of one GEMM launch and the kernel that runs it.
 struct GemmPlan {
-  int bm, bn, splits;
-  int dma = 0;  // 1: bf16 direct-to-LDS kernel (gemm_dma.hip)
+  int bm, bn;
+  int dma = 0;  // 1: bf16 direct-to-LDS kernel (gemm_dma.hip), else the register-staged kernel
 };
 template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus);
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 void gemm_bf16_dma(const GemmParams& p, const GemmPlan& g, hipStream_t s);
-size_t gemm_workspace_floats(const GemmPlan& g, int M, int N);
-size_t gemm_counters(const GemmPlan& g, int M, int N);
 template <typename T> constexpr int gemm_bk() { return sizeof(T) == 2 ? 64 : 32; }
 
 // ---------------------------------------------------------------- attention

@@ -320,10 +320,6 @@ struct Model {
   float *feat = nullptr, *hid = nullptr, *temb = nullptr, *tproj = nullptr;
   double* abar = nullptr;
   int cus = 256;                 // compute units of the device (GEMM planning)
-  float* gemm_ws = nullptr;      // split-K partials
-  size_t gemm_ws_floats = 0;
-  int* gemm_counters = nullptr;  // split-K arrival counters (self-resetting)
-  size_t gemm_n_counters = 0;
   void* zero = nullptr;          // 256 zero bytes: implicit-conv padding reads
   // shapes per layer output (for the executor)
   std::vector<int> act_h, act_w, act_c;
@@ -628,9 +624,6 @@ void size_workspace(Model* m, Sizer& z) {
 
 // ============================================================================ create / destroy
 
-// Split-K workspace of every GEMM one step and one call preparation launch
-// (defined after the executor).
-static void gemm_needs(Model* m, size_t* ws_floats, size_t* counters);
 
 Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats, bool on_device) {
   const std::vector<TensorSpec> table = weight_table(cfg);
@@ -728,12 +721,6 @@ Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats,
     DN_HIP(hipMemset(m->xin, 0, (size_t)m->n * HW0 * kCinPad * e));
     DN_HIP(hipMemset(m->zero, 0, 256));
     m->cus = prop.multiProcessorCount;
-    gemm_needs(m.get(), &m->gemm_ws_floats, &m->gemm_n_counters);
-    if (m->gemm_ws_floats) DN_HIP(hipMalloc(&m->gemm_ws, m->gemm_ws_floats * 4));
-    if (m->gemm_n_counters) {
-      DN_HIP(hipMalloc(&m->gemm_counters, m->gemm_n_counters * 4));
-      DN_HIP(hipMemset(m->gemm_counters, 0, m->gemm_n_counters * 4));
-    }
     abar_table(m->abar, cfg.n_train_steps, cfg.beta_start, cfg.beta_end, cfg.beta_schedule, s);
     DN_HIP(hipStreamSynchronize(s));
   } catch (...) {
@@ -750,8 +737,6 @@ void model_destroy(Model* m) {
   if (m->packed) (void)hipFree(m->packed);
   if (m->params) (void)hipFree(m->params);
   if (m->arena) (void)hipFree(m->arena);
-  if (m->gemm_ws) (void)hipFree(m->gemm_ws);
-  if (m->gemm_counters) (void)hipFree(m->gemm_counters);
   delete m;
 }
 
@@ -763,20 +748,11 @@ template <typename T> struct Exec {
   Model* m;
   hipStream_t s;
   int n;
-  bool dry = false;          // sizing pass: record workspace needs, launch nothing
-  size_t need_ws = 0, need_counters = 0;
+  bool dry = false;  // walk the step without launching anything
 
   void run_gemm(GemmParams& p) {
+    if (dry) return;
     const GemmPlan g = gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus);
-    if (dry) {
-      need_ws = std::max(need_ws, gemm_workspace_floats(g, p.M, p.N));
-      need_counters = std::max(need_counters, gemm_counters(g, p.M, p.N));
-      return;
-    }
-    p.ws = m->gemm_ws;
-    p.ws_floats = m->gemm_ws_floats;
-    p.counters = m->gemm_counters;
-    p.n_counters = m->gemm_n_counters;
     p.zero16 = m->zero;
     gemm<T>(p, g, s);
   }
@@ -1065,27 +1041,6 @@ void unet_eps_t(Model* m, const float* x, int t, const float* ctx, float scale, 
 }
 
 }  // namespace
-
-static void gemm_needs(Model* m, size_t* ws_floats, size_t* counters) {
-  size_t ws = 0, cnt = 0;
-  if (m->bf) {
-    Exec<bf16> ex{m, nullptr, m->n};
-    ex.dry = true;
-    ex.prepare(nullptr, 1);
-    ex.unet(0);
-    ws = ex.need_ws;
-    cnt = ex.need_counters;
-  } else {
-    Exec<float> ex{m, nullptr, m->n};
-    ex.dry = true;
-    ex.prepare(nullptr, 1);
-    ex.unet(0);
-    ws = ex.need_ws;
-    cnt = ex.need_counters;
-  }
-  *ws_floats = ws;
-  *counters = cnt;
-}
 
 void model_denoise(Model* m, float* latent, const float* ctx, const int32_t* ts, int n_ts, int start, int n,
                    float scale, hipStream_t s) {

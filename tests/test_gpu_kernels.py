@@ -33,8 +33,11 @@ def _rng(seed):
 
 
 @pytest.mark.parametrize("dtype", DT)
-@pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280)])
+@pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280),
+                                   (2048, 2048, 128), (8192, 512, 256)])
 def test_linear(dtype, M, N, K):
+    """Shapes cover every tile plan: 64 x 64 (few tiles), 128 x 128 (>= one tile per CU)
+    and, in bf16, the direct-to-LDS 256 x 256 kernel (M >= 8192 with a tile per CU)."""
     announce(f"linear dtype={dtype} M={M} N={N} K={K}")
     r = _rng(M + N + K)
     x, xh = to_dev(r.standard_normal((M, K)), dtype)
