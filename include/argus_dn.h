@@ -232,15 +232,26 @@ dn_status dn_op_conv3x3(int32_t dtype, const void* x, int32_t n, int32_t H, int3
                         void* y, int32_t Cout, int32_t y_f32, void* stream);
 
 /* Attention core O = softmax(Q K^T * scale) V for each (sample, head), the
- * score matrix never materialised: q [B][Sq][ldq], k [B][Skv][ldk],
- * v [B][Skv][ldv] (ldv == ldk), o [B][Sq][ldo]. Head h occupies columns
- * [h * head_stride, (h + 1) * head_stride), head_stride 32 or 64; a head of
- * d < head_stride real dimensions must hold zeros in its padding columns of
- * q and k (the padding columns of o then receive the same mix of v's padding
- * columns). Softmax in fp32. Asynchronous. */
-dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void* k, int32_t ldk, const void* v,
-                          int32_t ldv, void* o, int32_t ldo, int32_t B, int32_t heads, int32_t Sq, int32_t Skv,
+ * score matrix never materialised (flash-style, fp32 softmax):
+ * q [B][Sq][ldq], k [B][Skv][ldk], o [B][Sq][ldo]; head h occupies columns
+ * [h * head_stride, (h + 1) * head_stride) of each, head_stride 32 or 64.
+ * V is given transposed per head, as the projection GEMM writes it (see
+ * dn_op_linear_vt): vt [B][heads][head_stride][vt_ld], keys contiguous, with
+ * vt_ld >= Skv rounded up to 64 and finite values (e.g. zeros) in keys
+ * [Skv, vt_ld). A head of d < head_stride real dimensions must hold zeros in its
+ * padding columns of q and k. Asynchronous. */
+dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void* k, int32_t ldk, const void* vt,
+                          int32_t vt_ld, void* o, int32_t ldo, int32_t B, int32_t heads, int32_t Sq, int32_t Skv,
                           int32_t head_stride, float scale, void* stream);
+
+/* Attention input projection with the V part written transposed per head:
+ * acc[m][n] = sum_k x[m][k] * w[n][k] + bias[n] for n < N; columns n < vt_col0
+ * go to y [M][vt_col0] (e.g. Q and K), columns n >= vt_col0 (heads * head_stride
+ * of them) go to vt [M / seq][heads][head_stride][vt_ld] at token m % seq.
+ * Same kernels and tile plan as dn_op_linear. Asynchronous. */
+dn_status dn_op_linear_vt(int32_t dtype, const void* x, const void* w, const float* bias, void* y, int64_t M,
+                          int32_t N, int32_t K, int32_t vt_col0, void* vt, int32_t heads, int32_t head_stride,
+                          int32_t seq, int32_t vt_ld, void* stream);
 
 /* GroupNorm (Wu & He 2018) over NHWC x [n][HW][C] with G groups: biased
  * variance, statistics from fp32 partial sums merged in fp64,

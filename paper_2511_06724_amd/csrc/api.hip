@@ -257,29 +257,28 @@ dn_status dn_op_conv3x3(int32_t dtype, const void* x, int32_t n, int32_t H, int3
   });
 }
 
-dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void* k, int32_t ldk, const void* v,
-                          int32_t ldv, void* o, int32_t ldo, int32_t B, int32_t heads, int32_t Sq, int32_t Skv,
+dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void* k, int32_t ldk, const void* vt,
+                          int32_t vt_ld, void* o, int32_t ldo, int32_t B, int32_t heads, int32_t Sq, int32_t Skv,
                           int32_t head_stride, float scale, void* stream) {
   return guarded([&] {
     DN_CHECK(is_dtype(dtype), "dn_op_attention: bad dtype");
-    DN_CHECK(q && k && v && o, "dn_op_attention: null pointer");
+    DN_CHECK(q && k && vt && o, "dn_op_attention: null pointer");
     DN_CHECK(head_stride == 32 || head_stride == 64, "dn_op_attention: head_stride must be 32 or 64");
     DN_CHECK(B >= 1 && heads >= 1 && Sq >= 1 && Skv >= 1, "dn_op_attention: bad sizes");
-    DN_CHECK(ldq >= heads * head_stride && ldk >= heads * head_stride && ldv >= heads * head_stride &&
-                 ldo >= heads * head_stride,
+    DN_CHECK(ldq >= heads * head_stride && ldk >= heads * head_stride && ldo >= heads * head_stride,
              "dn_op_attention: leading dimension smaller than heads * head_stride");
+    DN_CHECK(vt_ld >= (Skv + 63) / 64 * 64, "dn_op_attention: vt_ld must cover Skv rounded up to 64");
     dn::AttnParams a;
     a.q = q;
     a.k = k;
-    a.v = v;
+    a.vt = vt;
     a.o = o;
     a.ldq = ldq;
     a.ldk = ldk;
-    a.ldv = ldv;
+    a.vt_ld = vt_ld;
     a.ldo = ldo;
     a.q_bs = (long long)Sq * ldq;
-    a.kv_bs = (long long)Skv * ldk;
-    DN_CHECK(ldk == ldv, "dn_op_attention: k and v must share a leading dimension");
+    a.k_bs = (long long)Skv * ldk;
     a.o_bs = (long long)Sq * ldo;
     a.B = B;
     a.heads = heads;
@@ -290,6 +289,44 @@ dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void*
       dn::attention<dn::bf16>(a, head_stride, as_stream(stream));
     else
       dn::attention<float>(a, head_stride, as_stream(stream));
+  });
+}
+
+dn_status dn_op_linear_vt(int32_t dtype, const void* x, const void* w, const float* bias, void* y, int64_t M,
+                          int32_t N, int32_t K, int32_t vt_col0, void* vt, int32_t heads, int32_t head_stride,
+                          int32_t seq, int32_t vt_ld, void* stream) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_op_linear_vt: bad dtype");
+    DN_CHECK(x && w && y && vt, "dn_op_linear_vt: null pointer");
+    DN_CHECK(M >= 1 && M <= 0x7fffffff && N >= 1 && K >= 1, "dn_op_linear_vt: bad sizes");
+    DN_CHECK(vt_col0 >= 4 && vt_col0 % 4 == 0 && vt_col0 < N, "dn_op_linear_vt: vt_col0 must be in [4, N), % 4 == 0");
+    DN_CHECK(head_stride >= 4 && head_stride % 4 == 0 && heads >= 1 && (N - vt_col0) == heads * head_stride,
+             "dn_op_linear_vt: N - vt_col0 must equal heads * head_stride (a multiple of 4)");
+    DN_CHECK(seq >= 1 && M % seq == 0 && vt_ld >= seq, "dn_op_linear_vt: rows must be whole sequences, vt_ld >= seq");
+    dn::GemmParams p;
+    p.a0 = x;
+    p.c0 = K;
+    p.lda0 = K;
+    p.taps = 1;
+    p.b = w;
+    p.ldb = K;
+    p.M = static_cast<int>(M);
+    p.N = N;
+    p.K = K;
+    p.bias = bias;
+    p.out = y;
+    p.ldo = vt_col0;
+    p.n_store = N;
+    p.vt = vt;
+    p.vt_col0 = vt_col0;
+    p.vt_dp = head_stride;
+    p.vt_heads = heads;
+    p.vt_seq = seq;
+    p.vt_ld = vt_ld;
+    if (dtype == DN_BF16)
+      op_gemm<dn::bf16>(p, as_stream(stream));
+    else
+      op_gemm<float>(p, as_stream(stream));
   });
 }
 

@@ -1,27 +1,34 @@
 // Flash-style multi-head attention for the UNet transformer blocks (gfx950).
 //
 // O = softmax(Q K^T * scale) V per (sample, head), never materialising the
-// score matrix: one workgroup = 4 waves = 128 queries of one (sample, head);
-// key/value tiles of 64 rows are staged in LDS (K row-major, V transposed) and
-// each wave runs an online softmax in fp32 over its 32 queries.
+// score matrix. A workgroup holds 32 queries per wave; key tiles of 64 rows of K
+// and the matching 64 columns of V^T (V stored transposed per head by the
+// projection GEMM, so both tiles are row-contiguous) are double-buffered in LDS:
+// the next tile's global loads are in flight while the current one is used.
 //
-// The wave computes S^T = K Q^T with 32x32 MFMA so that each lane owns one
-// query column of the score tile; the softmax row statistics are then a
-// per-lane reduction plus one exchange with the partner lane (lane ^ 32), and
-// the probabilities already sit in the B-operand layout of O^T = V^T P^T. The
-// V^T operand is read with the key permutation that matches the accumulator
-// layout, so no shuffle of P is needed.
+// Each wave computes S^T = K Q^T with 32x32 MFMA so that a lane owns one query
+// column: the softmax row statistics are a per-lane reduction plus one exchange
+// with the partner lane (lane ^ 32), and the probabilities already sit in the
+// B-operand layout of O^T = V^T P^T; the V^T operand is read with the key
+// permutation of the accumulator layout (two 8-byte reads per fragment).
+//
+// Lazy rescaling: the reference maximum m of a row is only moved (and O, l
+// rescaled by exp2(m_old - m_new)) when a tile's maximum exceeds it by more than
+// 2^8 in the exponent; otherwise probabilities up to 2^8 are accumulated against
+// the old reference. softmax(x) = exp(x - m) / sum exp(x - m) holds for any m, so
+// this changes rounding only, and saves the O rescale on most tiles.
 #include "kernels.h"
 
 namespace dn {
 namespace {
 
-constexpr int kKT = 64;  // keys per LDS tile
+constexpr int kKT = 64;          // keys per LDS tile
+constexpr float kLazy = 8.0f;    // log2 headroom before the reference max moves
 
 template <typename T> struct PvFrag;
 template <> struct PvFrag<bf16> {
-  // Keys of P registers [8c, 8c + 8) of a 32-key block for lane half h are
-  // 16c + 4h + {0..3} and 16c + 8 + 4h + {0..3}: two 8-byte LDS reads.
+  // P registers [8c, 8c + 8) of a 32-key block, lane half h, hold keys
+  // 16c + 4h + {0..3} and 16c + 8 + 4h + {0..3}.
   __device__ static __forceinline__ bf16x8 v(const bf16* vt_row, int kb, int c, int h) {
     const bf16* base = vt_row + kb * 32 + 16 * c + 4 * h;
     const bf16x4 lo = *reinterpret_cast<const bf16x4*>(base);
@@ -46,30 +53,33 @@ template <> struct PvFrag<float> {
   __device__ static __forceinline__ float p(const f32x16& s, int c) { return s[c]; }
 };
 
-template <typename T, int D>
-__global__ __launch_bounds__(256) void attn_kernel(AttnParams p) {
+template <typename T, int D, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_kernel(AttnParams p) {
   using MM = Mma<T>;
+  constexpr int NT = 64 * NW;
   constexpr int VEC = 16 / sizeof(T);
-  constexpr int SK = D + VEC;                      // K tile row stride
-  constexpr int SV = kKT + 8;                      // V^T row stride (keys)
+  constexpr int SK = D + VEC;                      // K tile row stride (elements)
+  constexpr int SV = kKT + VEC;                    // V^T tile row stride (keys)
   constexpr int NS = D / MM::KS;                   // MFMA steps over the head dim
   constexpr int DB = D / 32;                       // 32-row blocks of O^T
   constexpr int PCH = 16 / MM::KPL;                // MFMAs per 32-key block (P side)
-  constexpr int VPR = D / VEC;                     // 16-byte vectors per key row
+  constexpr int KV_VEC = kKT * D / VEC;            // 16-byte vectors per K tile (= per V^T tile)
+  constexpr int PER_T = (2 * KV_VEC + NT - 1) / NT;
+  constexpr int STAGE = kKT * SK + D * SV;
 
-  __shared__ __align__(16) T Ks[kKT * SK];
-  __shared__ __align__(16) T Vt[D * SV];
+  extern __shared__ __align__(16) unsigned char attn_smem[];
+  T* lds = reinterpret_cast<T*>(attn_smem);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int half = lane >> 5;
   const int b = blockIdx.z, h = blockIdx.y;
-  const int q0 = blockIdx.x * 128 + wave * 32;
+  const int q0 = blockIdx.x * (32 * NW) + wave * 32;
 
   const T* qp = static_cast<const T*>(p.q) + b * p.q_bs + h * D;
-  const T* kp = static_cast<const T*>(p.k) + b * p.kv_bs + h * D;
-  const T* vp = static_cast<const T*>(p.v) + b * p.kv_bs + h * D;
+  const T* kp = static_cast<const T*>(p.k) + b * p.k_bs + h * D;
+  const T* vtp = static_cast<const T*>(p.vt) + ((long long)b * p.heads + h) * D * p.vt_ld;
 
   const int qrow = min(q0 + (lane & 31), p.Sq - 1);
   typename MM::frag qf[NS];
@@ -81,21 +91,51 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnParams p) {
   for (int d = 0; d < DB; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[d][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_ref = -INFINITY, l_run = 0.f;
+
+  uint4 reg[PER_T];
+  auto load = [&](int t) {
+    const int k0 = t * kKT;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int v = tid + i * NT;
+      if (v < KV_VEC) {  // K row (key) kr, vector kc
+        const int kr = v / (D / VEC), kc = v - (v / (D / VEC)) * (D / VEC);
+        const long long key = min(k0 + kr, p.Skv - 1);
+        reg[i] = ld16(kp + key * p.ldk + kc * VEC);
+      } else if (v < 2 * KV_VEC) {  // V^T row d, keys [k0 + kc*VEC, +VEC)
+        const int w = v - KV_VEC;
+        const int d = w / (kKT / VEC), kc = w - (w / (kKT / VEC)) * (kKT / VEC);
+        reg[i] = ld16(vtp + (long long)d * p.vt_ld + k0 + kc * VEC);
+      }
+    }
+  };
+  auto store = [&](int buf) {
+    T* Ks = lds + buf * STAGE;
+    T* Vt = Ks + kKT * SK;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int v = tid + i * NT;
+      if (v < KV_VEC) {
+        const int kr = v / (D / VEC), kc = v - (v / (D / VEC)) * (D / VEC);
+        st16(Ks + kr * SK + kc * VEC, reg[i]);
+      } else if (v < 2 * KV_VEC) {
+        const int w = v - KV_VEC;
+        const int d = w / (kKT / VEC), kc = w - (w / (kKT / VEC)) * (kKT / VEC);
+        st16(Vt + d * SV + kc * VEC, reg[i]);
+      }
+    }
+  };
 
   const int ntiles = (p.Skv + kKT - 1) / kKT;
+  load(0);
+  store(0);
+  if (ntiles > 1) load(1);
+  __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
     const int k0 = t * kKT;
-    for (int i = tid; i < kKT * VPR; i += 256) {
-      const int kr = i / VPR, vcol = i - (i / VPR) * VPR;
-      const long long key = min(k0 + kr, p.Skv - 1);
-      st16(&Ks[kr * SK + vcol * VEC], ld16(kp + key * p.ldk + vcol * VEC));
-      const uint4 vv = ld16(vp + key * p.ldv + vcol * VEC);
-      const T* ve = reinterpret_cast<const T*>(&vv);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) Vt[(vcol * VEC + e) * SV + kr] = ve[e];
-    }
-    __syncthreads();
+    const T* Ks = lds + (t & 1) * STAGE;
+    const T* Vt = Ks + kKT * SK;
 
     f32x16 sacc[2];
 #pragma unroll
@@ -122,25 +162,27 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnParams p) {
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx * p.scale_log2);
-    const float alpha = exp2f(m_run - m_new);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+    if (__any(mx > m_ref + kLazy)) {
+      const float m_new = fmaxf(m_ref, mx);
+      const float alpha = exp2f(m_ref - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+      m_ref = m_new;
+    }
     float rs = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(sacc[kb][r] * p.scale_log2 - m_new);
+        const float e = exp2f(sacc[kb][r] * p.scale_log2 - m_ref);
         sacc[kb][r] = e;
         rs += e;
       }
-    rs += __shfl_xor(rs, 32, 64);
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int d = 0; d < DB; ++d)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+    l_run += rs + __shfl_xor(rs, 32, 64);
 
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -151,6 +193,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnParams p) {
         for (int d = 0; d < DB; ++d)
           o[d] = MM::mma(PvFrag<T>::v(&Vt[(d * 32 + (lane & 31)) * SV], kb, c, half), pf, o[d]);
       }
+
+    if (t + 1 < ntiles) {
+      store((t + 1) & 1);
+      if (t + 2 < ntiles) load(t + 2);
+    }
     __syncthreads();
   }
 
@@ -161,8 +208,27 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnParams p) {
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) op[d * 32 + acc_row(r, lane)] = from_f32<T>(o[d][r] * inv);
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[d][4 * g + e] * inv;
+        T* dst = op + d * 32 + 8 * g + 4 * half;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dst[e] = from_f32<T>(v[e]);
+      }
   }
+}
+
+template <typename T, int D, int NW> void launch(dim3 grid, const AttnParams& p, hipStream_t s) {
+  constexpr int VEC = 16 / sizeof(T);
+  const size_t lds = size_t(2) * (kKT * (D + VEC) + D * (kKT + VEC)) * sizeof(T);
+  static bool attr_set = false;
+  if (!attr_set) {
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, D, NW>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((attn_kernel<T, D, NW>), grid, dim3(64 * NW), lds, s, p);
 }
 
 }  // namespace
@@ -170,14 +236,26 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnParams p) {
 template <typename T> void attention(const AttnParams& p, int D, hipStream_t s) {
   DN_CHECK(p.B >= 1 && p.heads >= 1 && p.Sq >= 1 && p.Skv >= 1, "attention: empty problem");
   DN_CHECK(D == 32 || D == 64, "attention: padded head dim must be 32 or 64");
-  DN_CHECK(p.q && p.k && p.v && p.o, "attention: null operand");
+  DN_CHECK(p.q && p.k && p.vt && p.o, "attention: null operand");
   constexpr int VEC = 16 / sizeof(T);
-  DN_CHECK(p.ldq % VEC == 0 && p.ldk % VEC == 0 && p.ldv % VEC == 0, "attention: strides must be 16-byte multiples");
-  dim3 grid((p.Sq + 127) / 128, p.heads, p.B);
-  if (D == 64)
-    hipLaunchKernelGGL((attn_kernel<T, 64>), grid, dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL((attn_kernel<T, 32>), grid, dim3(256), 0, s, p);
+  DN_CHECK(p.ldq % VEC == 0 && p.ldk % VEC == 0 && p.vt_ld % VEC == 0, "attention: strides must be 16-byte multiples");
+  DN_CHECK(p.vt_ld >= (p.Skv + kKT - 1) / kKT * kKT, "attention: V^T rows must cover whole 64-key tiles");
+  // Fewer, wider workgroups when there are many queries; two waves per workgroup
+  // otherwise, so that short sequences still spread over every CU.
+  const long long wg4 = (long long)((p.Sq + 127) / 128) * p.heads * p.B;
+  if (wg4 >= 512) {
+    dim3 grid((p.Sq + 127) / 128, p.heads, p.B);
+    if (D == 64)
+      launch<T, 64, 4>(grid, p, s);
+    else
+      launch<T, 32, 4>(grid, p, s);
+  } else {
+    dim3 grid((p.Sq + 63) / 64, p.heads, p.B);
+    if (D == 64)
+      launch<T, 64, 2>(grid, p, s);
+    else
+      launch<T, 32, 2>(grid, p, s);
+  }
   DN_HIP(hipGetLastError());
 }
 

@@ -18,100 +18,13 @@
 // Work distribution: tiles are numbered so that each XCD (consecutive
 // workgroup ids go round-robin over the 8 XCDs) works through a contiguous band
 // of output columns with all row tiles, keeping that band of B in its L2.
-#include "kernels.h"
+#include "gemm_epilogue.h"
 
 namespace dn {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kXcds = 8;
-
-template <typename T> struct OutVec;
-template <> struct OutVec<bf16> {
-  __device__ static __forceinline__ void store(bf16* p, const float v[4]) {
-    bf16x4 o;
-    o[0] = static_cast<bf16>(v[0]);
-    o[1] = static_cast<bf16>(v[1]);
-    o[2] = static_cast<bf16>(v[2]);
-    o[3] = static_cast<bf16>(v[3]);
-    *reinterpret_cast<bf16x4*>(p) = o;
-  }
-  __device__ static __forceinline__ void load(const bf16* p, float v[4]) {
-    const bf16x4 i = *reinterpret_cast<const bf16x4*>(p);
-    v[0] = static_cast<float>(i[0]);
-    v[1] = static_cast<float>(i[1]);
-    v[2] = static_cast<float>(i[2]);
-    v[3] = static_cast<float>(i[3]);
-  }
-};
-template <> struct OutVec<float> {
-  __device__ static __forceinline__ void store(float* p, const float v[4]) {
-    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-  }
-  __device__ static __forceinline__ void load(const float* p, float v[4]) {
-    const float4 i = *reinterpret_cast<const float4*>(p);
-    v[0] = i.x;
-    v[1] = i.y;
-    v[2] = i.z;
-    v[3] = i.w;
-  }
-};
-
-
-// Stores 4 consecutive output columns [n, n + 4) of row m (n % 4 == 0), masking
-// columns >= n_store element-wise when the group straddles the edge.
-template <typename T>
-__device__ __forceinline__ void store4(const GemmParams& p, int m, int n, float v[4], int n_store) {
-  const long long o = (long long)m * p.ldo + n;
-  const bool vec = n + 4 <= n_store && (p.ldo & 3) == 0;
-  if (p.out_f32) {
-    float* out = static_cast<float*>(p.out);
-    if (vec) {
-      OutVec<float>::store(out + o, v);
-    } else {
-      for (int e = 0; e < 4; ++e)
-        if (n + e < n_store) out[o + e] = v[e];
-    }
-  } else {
-    T* out = static_cast<T*>(p.out);
-    if (vec) {
-      OutVec<T>::store(out + o, v);
-    } else {
-      for (int e = 0; e < 4; ++e)
-        if (n + e < n_store) out[o + e] = from_f32<T>(v[e]);
-    }
-  }
-}
-
-template <typename T>
-__device__ __forceinline__ void epilogue_group(const GemmParams& p, int m, int n, float v[4]) {
-  // v holds acc[m][n..n+3]; adds bias, per-sample row vector, residual; stores.
-  if (n >= p.n_store) return;
-  const bool full = n + 4 <= p.n_store;
-  if (p.bias) {
-    for (int e = 0; e < 4; ++e) v[e] += (full || n + e < p.n_store) ? p.bias[n + e] : 0.f;
-  }
-  if (p.rowvec) {
-    const float* rv = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
-    for (int e = 0; e < 4; ++e) v[e] += (full || n + e < p.n_store) ? rv[e] : 0.f;
-  }
-  if (p.resid) {
-    const long long ro = (long long)m * p.ldr + n;
-    if (full && (p.ldr & 3) == 0) {
-      float r[4];
-      if (p.resid_f32)
-        OutVec<float>::load(static_cast<const float*>(p.resid) + ro, r);
-      else
-        OutVec<T>::load(static_cast<const T*>(p.resid) + ro, r);
-      for (int e = 0; e < 4; ++e) v[e] += r[e];
-    } else {
-      for (int e = 0; e < 4; ++e)
-        if (n + e < p.n_store)
-          v[e] += p.resid_f32 ? static_cast<const float*>(p.resid)[ro + e] : to_f32(static_cast<const T*>(p.resid)[ro + e]);
-    }
-  }
-  store4<T>(p, m, n, v, p.n_store);
-}
 
 template <typename T, int BM, int BN, bool CONV>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p, int mt, int nt) {

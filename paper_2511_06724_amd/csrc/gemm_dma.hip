@@ -14,7 +14,7 @@
 //    block instead, so the LDS tile needs no second pass;
 //  - MFMA 32x32x16 issued as C^T = B A^T (four consecutive output columns per
 //    lane in the epilogue), XCD-aware tile order as in gemm.hip.
-#include "kernels.h"
+#include "gemm_epilogue.h"
 
 namespace dn {
 namespace {
@@ -33,65 +33,6 @@ constexpr int wait_vm_lgkm0(int vm) { return (vm & 0xF) | (((vm >> 4) & 3) << 14
 
 __device__ __forceinline__ int swz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
 
-
-__device__ __forceinline__ void store4_bf16(const GemmParams& p, int m, int n, const float v[4]) {
-  const long long o = (long long)m * p.ldo + n;
-  const bool vec = n + 4 <= p.n_store && (p.ldo & 3) == 0;
-  if (p.out_f32) {
-    float* out = static_cast<float*>(p.out);
-    if (vec) {
-      *reinterpret_cast<float4*>(out + o) = make_float4(v[0], v[1], v[2], v[3]);
-    } else {
-      for (int e = 0; e < 4; ++e)
-        if (n + e < p.n_store) out[o + e] = v[e];
-    }
-  } else {
-    bf16* out = static_cast<bf16*>(p.out);
-    if (vec) {
-      bf16x4 w;
-      w[0] = static_cast<bf16>(v[0]);
-      w[1] = static_cast<bf16>(v[1]);
-      w[2] = static_cast<bf16>(v[2]);
-      w[3] = static_cast<bf16>(v[3]);
-      *reinterpret_cast<bf16x4*>(out + o) = w;
-    } else {
-      for (int e = 0; e < 4; ++e)
-        if (n + e < p.n_store) out[o + e] = static_cast<bf16>(v[e]);
-    }
-  }
-}
-
-__device__ __forceinline__ void epilogue4(const GemmParams& p, int m, int n, float v[4]) {
-  if (n >= p.n_store) return;
-  const bool full = n + 4 <= p.n_store;
-  if (p.bias)
-    for (int e = 0; e < 4; ++e) v[e] += (full || n + e < p.n_store) ? p.bias[n + e] : 0.f;
-  if (p.rowvec) {
-    const float* rv = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
-    for (int e = 0; e < 4; ++e) v[e] += (full || n + e < p.n_store) ? rv[e] : 0.f;
-  }
-  if (p.resid) {
-    const long long ro = (long long)m * p.ldr + n;
-    if (full && (p.ldr & 3) == 0) {
-      if (p.resid_f32) {
-        const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(p.resid) + ro);
-        v[0] += r.x;
-        v[1] += r.y;
-        v[2] += r.z;
-        v[3] += r.w;
-      } else {
-        const bf16x4 r = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(p.resid) + ro);
-        for (int e = 0; e < 4; ++e) v[e] += static_cast<float>(r[e]);
-      }
-    } else {
-      for (int e = 0; e < 4; ++e)
-        if (n + e < p.n_store)
-          v[e] += p.resid_f32 ? static_cast<const float*>(p.resid)[ro + e]
-                              : static_cast<float>(static_cast<const bf16*>(p.resid)[ro + e]);
-    }
-  }
-  store4_bf16(p, m, n, v);
-}
 
 template <int BM, int BN, int WGM, int WGN, bool CONV>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmParams p, int mt, int nt) {
@@ -274,7 +215,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmParams p, 
         for (int g = 0; g < 4; ++g) {
           const int n = n0 + wn * WN + j * 32 + 8 * g + h4;
           float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-          epilogue4(p, m, n, v);
+          epilogue_group<bf16>(p, m, n, v);
         }
     }
   } else {
@@ -296,7 +237,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmParams p, 
             const float gg = acc[i][2 * j + 1][4 * g + e] + (p.bias ? p.bias[nv + 32 + e] : 0.f);
             v[e] = a * gelu_erf(gg);
           }
-          store4_bf16(p, m, o, v);
+          store4<bf16>(p, m, o, v, p.n_store);
         }
     }
   }

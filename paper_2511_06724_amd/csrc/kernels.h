@@ -38,6 +38,11 @@ struct GemmParams {
   int n_store = 0;  // output columns written
   int geglu = 0;
   const void* zero16 = nullptr;  // >= 16 zero bytes (implicit-conv padding reads, direct-to-LDS path)
+  // Transposed V output: columns n >= vt_col0 (the V projection of an attention,
+  // heads of vt_dp columns) are written to vt[sample][head][d][token] with token
+  // stride 1 and d stride vt_ld; rows are tokens, vt_seq per sample.
+  void* vt = nullptr;
+  int vt_col0 = 0, vt_dp = 0, vt_heads = 0, vt_seq = 1, vt_ld = 0;
 };
 
 // Block tile (bm x bn) of one GEMM launch and the kernel that runs it.
@@ -52,14 +57,16 @@ template <typename T> constexpr int gemm_bk() { return sizeof(T) == 2 ? 64 : 32;
 
 // ---------------------------------------------------------------- attention
 // O = softmax(Q K^T * scale) V per (sample, head). Head h occupies columns
-// [h*D, h*D + D) of q, k, v and o (D = 32 or 64).
+// [h*D, h*D + D) of q, k and o (D = 32 or 64); V is given transposed per head:
+// vt[((b * heads + h) * D + d) * vt_ld + key], vt_ld >= Skv rounded up to 64
+// (keys past Skv must hold finite values; they get zero weight).
 struct AttnParams {
   const void* q = nullptr;
   const void* k = nullptr;
-  const void* v = nullptr;
+  const void* vt = nullptr;
   void* o = nullptr;
-  int ldq = 0, ldk = 0, ldv = 0, ldo = 0;
-  long long q_bs = 0, kv_bs = 0, o_bs = 0;  // per-sample strides (elements)
+  int ldq = 0, ldk = 0, ldo = 0, vt_ld = 0;
+  long long q_bs = 0, k_bs = 0, o_bs = 0;  // per-sample strides (elements)
   int B = 0, heads = 0, Sq = 0, Skv = 0;
   float scale_log2 = 0.f;  // scale * log2(e)
 };

@@ -313,7 +313,10 @@ struct Model {
   float* R = nullptr;       // transformer residual stream fp32
   void *a = nullptr, *qkv = nullptr, *o = nullptr, *q2 = nullptr, *ff = nullptr, *rt = nullptr;
   void* kv = nullptr;       // [slots][n * ctx_len][2P_max]
-  size_t kv_slot_elems = 0;
+  size_t kv_slot_elems = 0;    // context keys per cross-attention: [n * ctx_len][P]
+  void* vt_self = nullptr;     // self-attention V^T [n][heads][Dp][round_up(HW, 64)]
+  void* vt_ctx = nullptr;      // context V^T per cross-attention [n][heads][Dp][round_up(ctx_len, 64)]
+  size_t vt_ctx_slot_elems = 0;
   void* ctx_t = nullptr;
   float* eps = nullptr;     // UNet output NHWC fp32
   float *gn_partial = nullptr, *gn_stats = nullptr;
@@ -541,7 +544,7 @@ namespace {
 
 struct Sizer {
   size_t gn_out = 0, c1 = 0, skip = 0, R = 0, a = 0, qkv = 0, o = 0, q2 = 0, ff = 0, kvslot = 0, gn_partial = 0,
-         gn_stats = 0;
+         gn_stats = 0, vt_self = 0, vt_ctx = 0;
   std::vector<size_t> acts;  // elements per main-path activation
 };
 
@@ -592,11 +595,13 @@ void size_workspace(Model* m, Sizer& z) {
         gn(HW, x.c);
         z.R = std::max(z.R, (size_t)n * HW * x.c);
         z.a = std::max(z.a, (size_t)n * HW * x.c);
-        z.qkv = std::max(z.qkv, (size_t)n * HW * 3 * P);
+        z.qkv = std::max(z.qkv, (size_t)n * HW * 2 * P);
+        z.vt_self = std::max(z.vt_self, (size_t)n * P * ((HW + 63) / 64 * 64));
+        z.vt_ctx = std::max(z.vt_ctx, (size_t)n * P * ((c.ctx_len + 63) / 64 * 64));
         z.o = std::max(z.o, (size_t)n * HW * P);
         z.q2 = std::max(z.q2, (size_t)n * HW * P);
         z.ff = std::max(z.ff, (size_t)n * HW * c.ff_mult * x.c);
-        z.kvslot = std::max(z.kvslot, (size_t)n * c.ctx_len * 2 * P);
+        z.kvslot = std::max(z.kvslot, (size_t)n * c.ctx_len * P);
         produce(H, W, ch);
         break;
       }
@@ -700,6 +705,9 @@ Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats,
     want.push_back({&m->ff, std::max<size_t>(z.ff, 1) * e});
     m->kv_slot_elems = z.kvslot;
     want.push_back({&m->kv, std::max<size_t>(z.kvslot * m->n_kv_slots, 1) * e});
+    m->vt_ctx_slot_elems = z.vt_ctx;
+    want.push_back({&m->vt_ctx, std::max<size_t>(z.vt_ctx * m->n_kv_slots, 1) * e});
+    want.push_back({&m->vt_self, std::max<size_t>(z.vt_self, 1) * e});
     want.push_back({&m->ctx_t, (size_t)m->n * cfg.ctx_len * cfg.ctx_dim * e});
     want.push_back({reinterpret_cast<void**>(&m->eps), (size_t)m->n * HW0 * cfg.latent_c * 4});
     want.push_back({reinterpret_cast<void**>(&m->gn_partial), z.gn_partial * 4});
@@ -720,6 +728,9 @@ Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats,
     }
     DN_HIP(hipMemset(m->xin, 0, (size_t)m->n * HW0 * kCinPad * e));
     DN_HIP(hipMemset(m->zero, 0, 256));
+    // V^T rows are padded to whole 64-key tiles; the padding must hold finite values.
+    DN_HIP(hipMemset(m->vt_ctx, 0, std::max<size_t>(z.vt_ctx * m->n_kv_slots, 1) * e));
+    DN_HIP(hipMemset(m->vt_self, 0, std::max<size_t>(z.vt_self, 1) * e));
     m->cus = prop.multiProcessorCount;
     abar_table(m->abar, cfg.n_train_steps, cfg.beta_start, cfg.beta_end, cfg.beta_schedule, s);
     DN_HIP(hipStreamSynchronize(s));
@@ -789,9 +800,15 @@ template <typename T> struct Exec {
     run_gemm(p);
   }
 
+  // Columns >= col0 of a projection written as per-head V^T (see GemmParams::vt).
+  struct VtOut {
+    void* vt = nullptr;
+    int col0 = 0, dp = 0, heads = 0, seq = 1, ld = 0;
+  };
+
   void linear(const LinW& w, const void* x, int ldx, long long M, void* out, int ldo, bool out_f32,
               const void* resid = nullptr, int ldr = 0, bool resid_f32 = false, bool geglu = false,
-              const void* x1 = nullptr, int c0 = 0, int c1 = 0) {
+              const void* x1 = nullptr, int c0 = 0, int c1 = 0, const VtOut& vt = VtOut()) {
     GemmParams p;
     p.a0 = x;
     p.a1 = x1;
@@ -814,6 +831,12 @@ template <typename T> struct Exec {
     p.out_f32 = out_f32;
     p.geglu = geglu;
     p.n_store = geglu ? w.n / 2 : w.n;
+    p.vt = vt.vt;
+    p.vt_col0 = vt.col0;
+    p.vt_dp = vt.dp;
+    p.vt_heads = vt.heads;
+    p.vt_seq = vt.seq;
+    p.vt_ld = vt.ld;
     run_gemm(p);
   }
 
@@ -851,19 +874,19 @@ template <typename T> struct Exec {
     conv(r.conv2, m->gn_out, H, W, 0, 1, out, H, W, nullptr, resid, false, r.cout, r.cout);
   }
 
-  void attention_(const void* q, int ldq, long long q_bs, const void* k, const void* v, int ldkv, long long kv_bs,
-                  int Sq, int Skv, const TxL& x) {
+  void attention_(const void* q, int ldq, long long q_bs, const void* k, int ldk, long long k_bs, const void* vt,
+                  int vt_ld, int Sq, int Skv, const TxL& x) {
     AttnParams a;
     a.q = q;
     a.k = k;
-    a.v = v;
+    a.vt = vt;
     a.o = m->o;
     a.ldq = ldq;
-    a.ldk = ldkv;
-    a.ldv = ldkv;
+    a.ldk = ldk;
+    a.vt_ld = vt_ld;
     a.ldo = x.heads * x.Dp;
     a.q_bs = q_bs;
-    a.kv_bs = kv_bs;
+    a.k_bs = k_bs;
     a.o_bs = (long long)Sq * x.heads * x.Dp;
     a.B = n;
     a.heads = x.heads;
@@ -883,16 +906,26 @@ template <typename T> struct Exec {
       const TxBlock& b = x.blocks[bi];
       const bool last = bi + 1 == x.blocks.size();
       if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln1.g, b.ln1.b, m->cfg.ln_eps, s);
-      linear(b.qkv, m->a, C, M, m->qkv, 3 * P, false);
+      // Q and K land in qkv [M][2P]; V goes to vt_self transposed per head.
+      const int ld_self = (HW + 63) / 64 * 64;
+      VtOut vs;
+      vs.vt = m->vt_self;
+      vs.col0 = 2 * P;
+      vs.dp = x.Dp;
+      vs.heads = x.heads;
+      vs.seq = HW;
+      vs.ld = ld_self;
+      linear(b.qkv, m->a, C, M, m->qkv, 2 * P, false, nullptr, 0, false, false, nullptr, 0, 0, vs);
       const char* qkv = static_cast<const char*>(m->qkv);
-      attention_(qkv, 3 * P, (long long)HW * 3 * P, qkv + (size_t)P * e, qkv + (size_t)2 * P * e, 3 * P,
-                 (long long)HW * 3 * P, HW, HW, x);
+      attention_(qkv, 2 * P, (long long)HW * 2 * P, qkv + (size_t)P * e, 2 * P, (long long)HW * 2 * P, m->vt_self,
+                 ld_self, HW, HW, x);
       linear(b.o1, m->o, P, M, m->R, C, true, m->R, C, true);
       if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln2.g, b.ln2.b, m->cfg.ln_eps, s);
       linear(b.q2, m->a, C, M, m->q2, P, false);
       const char* kv = static_cast<const char*>(m->kv) + (size_t)b.kv_slot * m->kv_slot_elems * e;
-      attention_(m->q2, P, (long long)HW * P, kv, kv + (size_t)P * e, 2 * P, (long long)m->cfg.ctx_len * 2 * P, HW,
-                 m->cfg.ctx_len, x);
+      const char* vtc = static_cast<const char*>(m->vt_ctx) + (size_t)b.kv_slot * m->vt_ctx_slot_elems * e;
+      attention_(m->q2, P, (long long)HW * P, kv, P, (long long)m->cfg.ctx_len * P, vtc,
+                 (m->cfg.ctx_len + 63) / 64 * 64, HW, m->cfg.ctx_len, x);
       linear(b.o2, m->o, P, M, m->R, C, true, m->R, C, true);
       if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln3.g, b.ln3.b, m->cfg.ln_eps, s);
       linear(b.ff1, m->a, C, M, m->ff, m->cfg.ff_mult * C, false, nullptr, 0, false, true);
@@ -922,7 +955,15 @@ template <typename T> struct Exec {
     for (const auto& x : m->tx)
       for (const auto& b : x.blocks) {
         void* dst = static_cast<char*>(m->kv) + (size_t)b.kv_slot * m->kv_slot_elems * sizeof(T);
-        linear(b.kv2, m->ctx_t, c.ctx_dim, (long long)n * c.ctx_len, dst, b.kv2.n, false);
+        VtOut vc;
+        vc.vt = static_cast<char*>(m->vt_ctx) + (size_t)b.kv_slot * m->vt_ctx_slot_elems * sizeof(T);
+        vc.col0 = b.kv2.n / 2;
+        vc.dp = x.Dp;
+        vc.heads = x.heads;
+        vc.seq = c.ctx_len;
+        vc.ld = (c.ctx_len + 63) / 64 * 64;
+        linear(b.kv2, m->ctx_t, c.ctx_dim, (long long)n * c.ctx_len, dst, b.kv2.n / 2, false, nullptr, 0, false,
+               false, nullptr, 0, 0, vc);
       }
   }
 

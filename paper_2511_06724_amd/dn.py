@@ -23,7 +23,7 @@ MAX_LEVELS = 4
 
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_unet_eps", "ac_lookup",
             "ac_fetch_latent", "dn_op_linear", "dn_op_conv3x3", "dn_op_attention", "dn_op_groupnorm",
-            "dn_op_layernorm", "dn_destroy", "dn_last_error")
+            "dn_op_layernorm", "dn_op_linear_vt", "dn_destroy", "dn_last_error")
 
 
 class DnError(RuntimeError):
@@ -70,6 +70,7 @@ def _load():
         "dn_op_linear": [I32, P, P, P, P, I32, P, I32, I64, I32, I32, I32, P],
         "dn_op_conv3x3": [I32, P, I32, I32, I32, I32, I32, I32, P, P, P, P, P, I32, I32, P],
         "dn_op_attention": [I32, P, I32, P, I32, P, I32, P, I32, I32, I32, I32, I32, I32, F32, P],
+        "dn_op_linear_vt": [I32, P, P, P, P, I64, I32, I32, I32, P, I32, I32, I32, I32, P],
         "dn_op_groupnorm": [I32, P, P, I32, I32, I32, I32, P, P, F32, I32],
         "dn_op_layernorm": [I32, P, P, I64, I32, P, P, F32, P],
         "dn_destroy": [P],
@@ -217,9 +218,14 @@ def op_conv3x3(dtype, x, n, H, W, Cin, w, bias, y, Cout, up=0, stride=1, temb=No
                              _ptr(resid), _ptr(y), Cout, int(y_f32), _stream(stream)))
 
 
-def op_attention(dtype, q, ldq, k, ldk, v, ldv, o, ldo, B, heads, Sq, Skv, head_stride, scale, stream=None):
-    _check(lib.dn_op_attention(dtype, _ptr(q), ldq, _ptr(k), ldk, _ptr(v), ldv, _ptr(o), ldo, B, heads, Sq, Skv,
+def op_attention(dtype, q, ldq, k, ldk, vt, vt_ld, o, ldo, B, heads, Sq, Skv, head_stride, scale, stream=None):
+    _check(lib.dn_op_attention(dtype, _ptr(q), ldq, _ptr(k), ldk, _ptr(vt), vt_ld, _ptr(o), ldo, B, heads, Sq, Skv,
                                head_stride, scale, _stream(stream)))
+
+
+def op_linear_vt(dtype, x, w, bias, y, M, N, K, vt_col0, vt, heads, head_stride, seq, vt_ld, stream=None):
+    _check(lib.dn_op_linear_vt(dtype, _ptr(x), _ptr(w), _ptr(bias), _ptr(y), M, N, K, vt_col0, _ptr(vt), heads,
+                               head_stride, seq, vt_ld, _stream(stream)))
 
 
 def op_groupnorm(dtype, x, y, n, HW, Cc, G, gamma, beta, eps, silu):

@@ -117,25 +117,35 @@ def _pad_heads(a, heads, d, dp):
     return out
 
 
+def _vt_layout(v, heads, dp, ld):
+    """[B, S, heads*dp] -> V^T [B, heads, dp, ld] (zeros past S)."""
+    B, S, _ = v.shape
+    out = np.zeros((B, heads, dp, ld), dtype=v.dtype)
+    out[..., :S] = v.reshape(B, S, heads, dp).transpose(0, 2, 3, 1)
+    return out
+
+
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("B,heads,Sq,Skv,d", [(2, 3, 200, 77, 64), (1, 2, 256, 300, 64), (2, 2, 130, 96, 40),
-                                              (2, 4, 256, 256, 16), (1, 1, 5, 1, 64)])
+                                              (2, 4, 256, 256, 16), (1, 1, 5, 1, 64), (2, 20, 1024, 1024, 64)])
 def test_attention(dtype, B, heads, Sq, Skv, d):
     announce(f"attention dtype={dtype} B={B} heads={heads} Sq={Sq} Skv={Skv} d={d}")
     r = _rng(B * heads + Sq + Skv + d)
     dp = 32 if d <= 32 else 64
+    ld = (Skv + 63) // 64 * 64
     q = r.standard_normal((B, Sq, heads * d)).astype(np.float32)
     k = r.standard_normal((B, Skv, heads * d)).astype(np.float32)
     v = r.standard_normal((B, Skv, heads * d)).astype(np.float32)
     qd, qh = to_dev(_pad_heads(q, heads, d, dp), dtype)
     kd, kh = to_dev(_pad_heads(k, heads, d, dp), dtype)
-    vd, vh = to_dev(_pad_heads(v, heads, d, dp), dtype)
+    vtd, vth = to_dev(_vt_layout(_pad_heads(v, heads, d, dp), heads, dp, ld), dtype)
     o = torch.zeros((B, Sq, heads * dp), device=DEV, dtype=tdtype(dtype))
     P = heads * dp
-    dn.op_attention(dtype, qd, P, kd, P, vd, P, o, P, B, heads, Sq, Skv, dp, 1.0 / math.sqrt(d))
+    dn.op_attention(dtype, qd, P, kd, P, vtd, ld, o, P, B, heads, Sq, Skv, dp, 1.0 / math.sqrt(d))
     torch.cuda.synchronize()
     # oracle: multi-head attention with identity projections on the unpadded heads
     strip = lambda a: np.concatenate([a[..., h * dp:h * dp + d] for h in range(heads)], axis=-1)
+    vh = vth[..., :Skv].transpose(0, 3, 1, 2).reshape(B, Skv, P)            # back to [B, Skv, heads*dp]
     c = heads * d
     eye, zero = np.eye(c), np.zeros((c, c))
     xkv = np.concatenate([strip(kh), strip(vh)], axis=-1)          # K and V from one [.., 2c] input
@@ -145,6 +155,33 @@ def test_attention(dtype, B, heads, Sq, Skv, d):
     # padding columns of o are zero (v's padding is zero)
     if dp != d:
         assert np.all(got[..., d:dp] == 0)
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("M,seq,heads,dp,K", [(300, 150, 3, 64, 128), (512, 256, 4, 32, 64), (8192, 4096, 10, 64, 640),
+                                              (2048, 1024, 20, 64, 1280)])
+def test_linear_vt(dtype, M, seq, heads, dp, K):
+    """Attention input projection: Q, K columns to y, V columns transposed per head
+    into vt[sample][head][d][token] (the last two shapes are the SD-XL QKV projections,
+    the 8192-row one on the direct-to-LDS kernel)."""
+    announce(f"linear_vt dtype={dtype} M={M} seq={seq} heads={heads} dp={dp} K={K}")
+    P = heads * dp
+    N = 3 * P
+    r = _rng(M + K + dp)
+    x, xh = to_dev(r.standard_normal((M, K)), dtype)
+    w, wh = to_dev(r.standard_normal((N, K)) / math.sqrt(K), dtype)
+    b = r.standard_normal(N).astype(np.float32)
+    ld = (seq + 63) // 64 * 64
+    y = torch.empty((M, 2 * P), device=DEV, dtype=tdtype(dtype))
+    vt = torch.zeros((M // seq, heads, dp, ld), device=DEV, dtype=tdtype(dtype))
+    dn.op_linear_vt(dtype, x, w, f32_dev(b), y, M, N, K, 2 * P, vt, heads, dp, seq, ld)
+    torch.cuda.synchronize()
+    ref = L.linear(xh, wh, b.astype(np.float64))
+    assert rel_l2(host(y), ref[:, :2 * P]) < TOL[dtype]
+    ref_vt = ref[:, 2 * P:].reshape(M // seq, seq, heads, dp).transpose(0, 2, 3, 1)
+    got = host(vt)
+    assert rel_l2(got[..., :seq], ref_vt) < TOL[dtype]
+    assert np.all(got[..., seq:] == 0)
 
 
 @pytest.mark.parametrize("dtype", DT)
@@ -237,19 +274,21 @@ def test_sdxl_self_attention_sampled():
     B, heads, S, d = 2, 10, 4096, 64
     P = heads * d
     g = torch.Generator(device=DEV).manual_seed(5)
-    qkv = torch.randn((B, S, 3 * P), device=DEV, generator=g).to(torch.bfloat16)
+    qk = torch.randn((B, S, 2 * P), device=DEV, generator=g).to(torch.bfloat16)
+    vt = torch.randn((B, heads, d, S), device=DEV, generator=g).to(torch.bfloat16)
     o = torch.empty((B, S, P), device=DEV, dtype=torch.bfloat16)
-    q, k, v = qkv[..., :P], qkv[..., P:2 * P], qkv[..., 2 * P:]
-    dn.lib.dn_op_attention(dn.DN_BF16, q.data_ptr(), 3 * P, k.data_ptr(), 3 * P, v.data_ptr(), 3 * P, o.data_ptr(),
+    q, k = qk[..., :P], qk[..., P:]
+    dn.lib.dn_op_attention(dn.DN_BF16, q.data_ptr(), 2 * P, k.data_ptr(), 2 * P, vt.data_ptr(), S, o.data_ptr(),
                            P, B, heads, S, S, 64, 1.0 / 8.0, torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
     r = _rng(7)
-    qh = host(qkv)
+    qh = host(qk)
+    vh = host(vt)
     oh = host(o)
     for b, h in [(0, 0), (1, 9), (0, 5)]:
         rows = r.integers(0, S, size=16)
         K_ = qh[b, :, P + h * d:P + (h + 1) * d]
-        V_ = qh[b, :, 2 * P + h * d:2 * P + (h + 1) * d]
+        V_ = vh[b, h].T                                   # [S, d]
         for i in rows:
             s = K_ @ qh[b, i, h * d:(h + 1) * d] / 8.0
             p = np.exp(s - s.max())
