@@ -27,6 +27,31 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
+def kernel_source_hash():
+    """sha256 over the sources of the GEMM kernel the roofline reports (so that HBM
+    traffic measured with counters is only reported for the kernel it was taken on)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "gemm_epilogue.h", "common.h", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2511_06724_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the FF-in GEMM from profiles/ff_in_gemm_traffic.json
+    (FETCH_SIZE + WRITE_SIZE counter passes, scaled by a plain copy of known size),
+    or None when the file is missing or was taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", "ff_in_gemm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
 def unet_flops(cfg, n):
     """(conv + linear, attention) FLOPs of one UNet evaluation on n samples (2 per MAC)."""
     c0, temb = cfg.model_channels, 4 * cfg.model_channels
@@ -105,19 +130,35 @@ def roofline_ff_in(torch, dn, stream, iters=20):
     y = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
     for _ in range(3):
         dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True, stream=stream)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(iters):
+    # one event pair around each launch, on the stream the kernel runs on
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+    for e0, e1 in ev:
+        e0.record(stream)
         dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True, stream=stream)
-    e1.record(stream)
-    e1.synchronize()
-    avg_s = e0.elapsed_time(e1) / 1e3 / iters
+        e1.record(stream)
+    torch.cuda.synchronize()
+    avg_s = sum(e0.elapsed_time(e1) for e0, e1 in ev) / 1e3 / iters
     flops = 2.0 * M * (2 * N) * K
     achieved = flops / avg_s / 1e12
     return {"kernel": "gemm_kernel<bf16,128x128,linear> FF-in GEGLU 2048x10240x1280", "bound": "mfma",
             "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-            "avg_launch_us": round(avg_s * 1e6, 2), "flops_per_launch": flops}
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(),
+            "avg_launch_us": round(avg_s * 1e6, 2), "flops_per_launch": flops,
+            "kernel_source_hash": kernel_source_hash()}
+
+
+def profile_kernel(torch, dn):
+    """Counter-collection mode: 20 launches of the FF-in GEMM, then a plain device
+    copy of 256 MiB (its FETCH_SIZE / WRITE_SIZE calibrate the counters)."""
+    stream = torch.cuda.current_stream()
+    roofline_ff_in(torch, dn, stream)
+    a = torch.empty(64 << 20, device="cuda", dtype=torch.float32).fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_kernel": "done", "copy_bytes": a.numel() * 4,
+                      "kernel_source_hash": kernel_source_hash()}))
 
 
 def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, queries=4):
@@ -132,17 +173,33 @@ def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, queries
     for s in range(0, n_entries, 10_000):
         lat_cache[s:s + 10_000].normal_(generator=g)
     qd = [torch.from_numpy(q.view("uint16").copy()).cuda() for q in qs]
-    # lookup timing (warm: the 153.6 MB table is resident in the 256 MB last-level cache after one pass)
+    # warm: the 153.6 MB table stays in the 256 MB last-level cache between queries
     dn.ac_lookup(qd[0], cache)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    for _ in range(4):
+        for q in qd:
+            dn.ac_lookup(q, cache)
+    t_warm = (time.perf_counter() - t0) / (4 * len(qd))
+    # cold: a 1 GiB write between queries evicts the table from the last-level cache
+    flush = torch.empty(256 << 20, device="cuda", dtype=torch.float32)
+    t_cold = 0.0
     for q in qd:
-        idx, _ = dn.ac_lookup(q, cache)
-    t_lookup = (time.perf_counter() - t0) / len(qd)
+        flush.fill_(0.0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        dn.ac_lookup(q, cache)
+        t_cold += time.perf_counter() - t0
+    t_cold /= len(qd)
+    del flush
+    t_lookup = t_warm
     ok = all(dn.ac_lookup(q, cache)[0] == int(r) for q, r in zip(qd, rows))
     lat = torch.empty((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda")
-    out = {"lookup_us_per_query": round(t_lookup * 1e6, 1),
-           "lookup_GBps": round(n_entries * dim * 2 / t_lookup / 1e9, 1), "planted_found": ok, "k": {}}
+    out = {"lookup_us_per_query_warm": round(t_warm * 1e6, 1), "lookup_us_per_query_cold": round(t_cold * 1e6, 1),
+           "lookup_GBps_warm": round(n_entries * dim * 2 / t_warm / 1e9, 1),
+           "lookup_GBps_cold": round(n_entries * dim * 2 / t_cold / 1e9, 1),
+           "lookup_note": "synchronous call timed on the host (includes launch and the 16-byte result copy)",
+           "planted_found": ok, "queries_per_k": 2, "images_per_s_by_k": {}}
     for k in (0, 5, 10, 15, 20, 25):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -152,16 +209,18 @@ def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, queries
             model.denoise(lat, ctx, ts, k, 50 - k, 7.5)
         torch.cuda.synchronize()
         dt = (time.perf_counter() - t0) / 2
-        out["k"][str(k)] = round(1.0 / dt, 4)
+        out["images_per_s_by_k"][str(k)] = round(1.0 / dt, 4)
         print(f"[bench] ac k={k}: {1.0 / dt:.3f} images/s", file=sys.stderr, flush=True)
     del lat_cache
     return out
 
 
-def cpu_baseline(sample_blocks=4):
-    """The CPU oracle on the host cores: one SD-XL 32x32 transformer stage (C = 1280,
-    20 heads x 64, batch 2 with guidance) of `sample_blocks` blocks plus one top-level
-    ResBlock (128x128, C = 320), timed, then scaled by FLOPs to a full denoise step."""
+def cpu_baseline(budget_s=12.0):
+    """The CPU oracle on the host cores, on a bounded sample of the SD-XL step: one
+    top-level ResBlock (128x128, C = 320) and then single-block transformer stages at
+    the 32x32 level (C = 1280, 20 heads x 64, batch 2 with guidance, 77x2048 context)
+    until about `budget_s` seconds have passed; the FLOPs done per second are then
+    scaled to a full denoise step."""
     import numpy as np
     from oracle import unet as OU
     from paper_2511_06724_amd import workloads as W
@@ -169,13 +228,14 @@ def cpu_baseline(sample_blocks=4):
 
     threads = len(os.sched_getaffinity(0))
     cfg = W.sdxl()
-    sub = cfg.with_(levels=((320, 0, 5, 64), (640, 0, 10, 64), (1280, sample_blocks, 20, 64)))
+    sub = cfg.with_(levels=((320, 0, 5, 64), (640, 0, 10, 64), (1280, 1, 20, 64)))
     rng = np.random.default_rng(0)
-    names = [r for r in OT.tensor_table(sub) if r[0].startswith("down2.0.tx") or r[0].startswith("down0.0.res")]
     Wt = {}
-    for name, shape, kind, fan in names:
+    for name, shape, kind, fan in OT.tensor_table(sub):
+        if not (name.startswith("down2.0.tx") or name.startswith("down0.0.res")):
+            continue
         if kind in ("w", "b"):
-            Wt[name] = (rng.standard_normal(shape, dtype=np.float32) / np.float32(math.sqrt(fan)))
+            Wt[name] = rng.standard_normal(shape, dtype=np.float32) / np.float32(math.sqrt(fan))
         elif kind == "g":
             Wt[name] = 1 + 0.1 * rng.standard_normal(shape, dtype=np.float32)
         else:
@@ -184,22 +244,64 @@ def cpu_baseline(sample_blocks=4):
     x_res = rng.standard_normal((2, 320, 128, 128), dtype=np.float32)
     ctx = rng.standard_normal((2, 77, 2048), dtype=np.float32)
     temb = rng.standard_normal((2, 1280), dtype=np.float32)
-    t0 = time.perf_counter()
-    OU.transformer(sub, Wt, "down2.0.tx", x_tx, ctx, sample_blocks, 20)
-    OU.resblock(sub, Wt, "down0.0.res", x_res, temb)
-    dt = time.perf_counter() - t0
     hw, c, tok = 1024, 1280, 2048
-    tx_flops = 4 * tok * c * c + sample_blocks * (2 * tok * c * c * 18 + 4 * 2 * 77 * 2048 * c
-                                                   + 4 * 2 * hw * hw * c + 4 * 2 * hw * 77 * c)
+    tx_flops = 4 * tok * c * c + (2 * tok * c * c * 18 + 4 * 2 * 77 * 2048 * c + 4 * 2 * hw * hw * c
+                                  + 4 * 2 * hw * 77 * c)
     res_flops = 2 * 2 * 16384 * 320 * 9 * 640 + 2 * 2 * 1280 * 320
+    t0 = time.perf_counter()
+    OU.resblock(sub, Wt, "down0.0.res", x_res, temb)
+    done, blocks = res_flops, 0
+    while True:
+        OU.transformer(sub, Wt, "down2.0.tx", x_tx, ctx, 1, 20)
+        done += tx_flops
+        blocks += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
     lin, att = unet_flops(cfg, 2)
-    sample_flops = tx_flops + res_flops
-    steps_per_s = (sample_flops / dt) / (lin + att)
-    return {"value": round(steps_per_s, 6), "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": (f"one SD-XL 32x32 transformer stage of {sample_blocks} blocks + one 128x128 ResBlock "
-                       f"(batch 2), {sample_flops / 1e12:.3f} TFLOP in {dt:.1f} s, extrapolated by FLOPs to a "
-                       f"full {(lin + att) / 1e12:.3f} TFLOP step"),
+    steps_per_s = (done / dt) / (lin + att)
+    return {"value": round(steps_per_s, 6), "unit": "denoise steps/s", "cores": threads, "kind": "oracle",
+            "sample": (f"one SD-XL 128x128 ResBlock + {blocks} single-block 32x32 transformer stages (batch 2), "
+                       f"{done / 1e12:.3f} TFLOP in {dt:.1f} s on {threads} host threads, extrapolated by FLOPs to a "
+                       f"full {(lin + att) / 1e12:.3f} TFLOP denoise step"),
             "images_per_s": round(steps_per_s / 50, 8)}
+
+
+def time_images(torch, model, cfg, ts, images, warmup=1):
+    g = torch.Generator(device="cuda").manual_seed(0)
+    x0 = torch.randn((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda", generator=g)
+    ctx = torch.randn((2 * cfg.batch, cfg.ctx_len, cfg.ctx_dim), device="cuda", generator=g)
+    lat = x0.clone()
+    for _ in range(warmup):
+        lat.copy_(x0)
+        model.denoise(lat, ctx, ts, 0, 50, 7.5)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(images):
+        lat.copy_(x0)
+        model.denoise(lat, ctx, ts, 0, 50, 7.5)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / images
+
+
+def sweep_batch(torch, dn, W, args):
+    import numpy as np
+    ts = np.array([(49 - j) * 20 + 1 for j in range(50)] + [-1], np.int32)
+    cases = [("sdxl", b, W.sdxl(W.DN_BF16, batch=b)) for b in (1, 2, 4, 8)]
+    cases += [("sdxl_small", 1, W.sdxl_small(W.DN_BF16, batch=1))]
+    for name, b, cfg in cases:
+        blob = device_weights(torch, dn, cfg, seed=42)
+        model = dn.Denoiser(cfg, blob)
+        del blob
+        torch.cuda.empty_cache()
+        sec = time_images(torch, model, cfg, ts, images=max(1, args.steps // b), warmup=1)
+        lin, att = unet_flops(cfg, 2 * b)
+        print(json.dumps({"variant": name, "batch": b, "latency_s_per_call": round(sec, 4),
+                          "images_per_s": round(b / sec, 4), "denoise_steps_per_s": round(50 / sec, 3),
+                          "tflop_per_step": round((lin + att) / 1e12, 3),
+                          "mfma_util": round((lin + att) * 50 / sec / 1e12 / PEAK_BF16_TFLOPS, 4)}), flush=True)
+        model.close()
+        torch.cuda.empty_cache()
 
 
 def main():
@@ -210,6 +312,11 @@ def main():
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ac", action="store_true")
+    ap.add_argument("--profile-kernel", action="store_true",
+                    help="only launch the FF-in GEMM 20 times and a 256 MiB copy (counter collection)")
+    ap.add_argument("--sweep-batch", action="store_true",
+                    help="instead of the headline line: latency and images/s for batch 1, 2, 4, 8 and the "
+                         "smaller variant (4 / 1 transformer blocks per 32x32 / 64x64 stage)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the denoise loop is replicated per GPU, "
@@ -221,6 +328,12 @@ def main():
 
     assert torch.cuda.is_available()
     torch.cuda.set_device(0)
+    if args.profile_kernel:
+        profile_kernel(torch, dn)
+        return
+    if args.sweep_batch:
+        sweep_batch(torch, dn, W, args)
+        return
     cfg = W.sdxl(W.DN_BF16, batch=args.batch)
     print("[bench] generating SD-XL weights on the device", file=sys.stderr, flush=True)
     blob = device_weights(torch, dn, cfg, seed=42)
