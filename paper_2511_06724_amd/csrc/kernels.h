@@ -49,6 +49,8 @@ struct GemmParams {
 struct GemmPlan {
   int bm, bn;
   int dma = 0;  // 1: bf16 direct-to-LDS kernel (gemm_dma.hip), else the register-staged kernel
+  int wgm = 2, wgn = 2;  // direct-to-LDS kernel: wave grid over the block tile
+  int stages = 2;        // direct-to-LDS kernel: LDS pipeline depth
 };
 template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus);
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s);
