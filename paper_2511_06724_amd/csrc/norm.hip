@@ -7,11 +7,13 @@
 //   2. finalize: one workgroup per (sample, group) merges the chunk partials in
 //      fp64 in a fixed order and writes per-(sample, channel) scale and shift
 //      (gamma * rstd, beta - mean * gamma * rstd);
-//   3. apply: y = x * scale + shift (then SiLU), one FMA per element.
+//   3. apply: y = x * scale + shift (then SiLU), one FMA per element, 16-byte
+//      vectors, a (pixel block, sample) grid.
 // The input may be the channel concatenation of two tensors (the up path's
 // [h, skip]); the output is always one contiguous tensor.
 //
-// LayerNorm: one wave per token row in registers, two-pass mean / variance.
+// LayerNorm: one wave per token row in registers, two-pass mean / variance,
+// 16-byte loads and 8-byte (bf16) stores.
 #include "kernels.h"
 
 namespace dn {
@@ -133,33 +135,76 @@ __global__ __launch_bounds__(256) void gn_finalize_kernel(GroupNormParams p, GnG
   }
 }
 
+// Apply: grid (pixel blocks, samples); a block covers kApplyPix pixels of one sample,
+// its threads walk the (pixel, 16-byte channel vector) pairs with an incremental
+// quotient / remainder (no division in the loop).
+constexpr int kApplyVecs = 2048;  // 16-byte vectors per apply workgroup (8 per thread)
+
 template <typename T>
-__global__ __launch_bounds__(256) void gn_apply_kernel(GroupNormParams p, GnGeom g) {
+__global__ __launch_bounds__(256) void gn_apply_kernel(GroupNormParams p, GnGeom g, int pix_per_block) {
   constexpr int VEC = Elem<T>::kVec;
-  const long long total = (long long)p.n * p.HW * g.V;
-  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
-    const long long pix = i / g.V;
-    const int vi = static_cast<int>(i - pix * g.V);
-    const int n = static_cast<int>(pix / p.HW);
-    int c = vi * VEC;
+  const int V = g.V;
+  const int n = blockIdx.y;
+  const int pix0 = blockIdx.x * pix_per_block;
+  const int npix = min(pix_per_block, p.HW - pix0);
+  const int step_q = 256 / V, step_r = 256 - (256 / V) * V;
+  int q = threadIdx.x / V, r = threadIdx.x - (threadIdx.x / V) * V;
+  const float* scale = p.stats + (long long)n * g.C;
+  const float* shift = p.stats + (long long)(p.n + n) * g.C;
+  const long long rowbase = (long long)n * p.HW + pix0;
+  for (; q < npix;) {
+    const long long pix = rowbase + q;
+    const int c = r * VEC;
     const uint4 raw = c < p.c0 ? ld16(static_cast<const T*>(p.x0) + pix * p.c0 + c)
                                : ld16(static_cast<const T*>(p.x1) + pix * p.c1 + (c - p.c0));
     const T* xv = reinterpret_cast<const T*>(&raw);
-    const float* sc = p.stats + (long long)n * g.C + c;
-    const float* sh = p.stats + (long long)(p.n + n) * g.C + c;
     uint4 outv;
     T* ov = reinterpret_cast<T*>(&outv);
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      float v = to_f32(xv[e]) * sc[e] + sh[e];
-      if (p.silu) v = silu_f(v);
-      ov[e] = from_f32<T>(v);
+    for (int e = 0; e < VEC; e += 4) {
+      const float4 sc = *reinterpret_cast<const float4*>(scale + c + e);
+      const float4 sh = *reinterpret_cast<const float4*>(shift + c + e);
+      float v0 = to_f32(xv[e + 0]) * sc.x + sh.x, v1 = to_f32(xv[e + 1]) * sc.y + sh.y;
+      float v2 = to_f32(xv[e + 2]) * sc.z + sh.z, v3 = to_f32(xv[e + 3]) * sc.w + sh.w;
+      if (p.silu) {
+        v0 = silu_f(v0);
+        v1 = silu_f(v1);
+        v2 = silu_f(v2);
+        v3 = silu_f(v3);
+      }
+      ov[e + 0] = from_f32<T>(v0);
+      ov[e + 1] = from_f32<T>(v1);
+      ov[e + 2] = from_f32<T>(v2);
+      ov[e + 3] = from_f32<T>(v3);
     }
     st16(static_cast<T*>(p.y) + pix * g.C + c, outv);
+    q += step_q;
+    r += step_r;
+    if (r >= V) {
+      r -= V;
+      ++q;
+    }
   }
 }
 
 constexpr int kLnMaxVec = 8;  // float4 vectors per lane: C <= 2048
+
+template <typename T> struct Store4;
+template <> struct Store4<bf16> {
+  __device__ static __forceinline__ void st(bf16* p, float a, float b, float c, float d) {
+    bf16x4 o;
+    o[0] = static_cast<bf16>(a);
+    o[1] = static_cast<bf16>(b);
+    o[2] = static_cast<bf16>(c);
+    o[3] = static_cast<bf16>(d);
+    *reinterpret_cast<bf16x4*>(p) = o;
+  }
+};
+template <> struct Store4<float> {
+  __device__ static __forceinline__ void st(float* p, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+  }
+};
 
 template <typename T>
 __global__ __launch_bounds__(256) void ln_kernel(const float* x, T* y, long long M, int C, const float* gamma,
@@ -191,15 +236,15 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* x, T* y, long long
   }
   const float rstd = rsqrtf(wave_sum(q) / C + eps);
   T* yr = y + row * C;
+  const float4* g4 = reinterpret_cast<const float4*>(gamma);
+  const float4* b4 = reinterpret_cast<const float4*>(beta);
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
     const int i = lane + 64 * j;
     if (i < nv) {
-      const int c = 4 * i;
-      yr[c + 0] = from_f32<T>((v[j].x - mean) * rstd * gamma[c + 0] + beta[c + 0]);
-      yr[c + 1] = from_f32<T>((v[j].y - mean) * rstd * gamma[c + 1] + beta[c + 1]);
-      yr[c + 2] = from_f32<T>((v[j].z - mean) * rstd * gamma[c + 2] + beta[c + 2]);
-      yr[c + 3] = from_f32<T>((v[j].w - mean) * rstd * gamma[c + 3] + beta[c + 3]);
+      const float4 g = g4[i], bb = b4[i];
+      Store4<T>::st(yr + 4 * i, (v[j].x - mean) * rstd * g.x + bb.x, (v[j].y - mean) * rstd * g.y + bb.y,
+                    (v[j].z - mean) * rstd * g.z + bb.z, (v[j].w - mean) * rstd * g.w + bb.w);
     }
   }
 }
@@ -224,9 +269,8 @@ template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s) {
   const GnGeom g = gn_geom<T>(p.HW, C);
   hipLaunchKernelGGL(gn_partial_kernel<T>, dim3(g.chunks, p.n, g.vslices), dim3(256), 0, s, p, g);
   hipLaunchKernelGGL(gn_finalize_kernel, dim3(p.G, p.n), dim3(256), 0, s, p, g);
-  const long long total = (long long)p.n * p.HW * g.V;
-  const int blocks = static_cast<int>(total / 256 + 1 < 8192 ? total / 256 + 1 : 8192);
-  hipLaunchKernelGGL(gn_apply_kernel<T>, dim3(blocks), dim3(256), 0, s, p, g);
+  const int ppb = (kApplyVecs + g.V - 1) / g.V;
+  hipLaunchKernelGGL(gn_apply_kernel<T>, dim3((p.HW + ppb - 1) / ppb, p.n), dim3(256), 0, s, p, g, ppb);
   DN_HIP(hipGetLastError());
 }
 
@@ -235,6 +279,8 @@ void layernorm(const float* x, T* y, long long M, int C, const float* gamma, con
                hipStream_t s) {
   DN_CHECK(M >= 1 && C >= 4 && C % 4 == 0 && C <= 4 * 64 * kLnMaxVec, "layernorm: C must be a multiple of 4, <= 2048");
   DN_CHECK(x && y && gamma && beta, "layernorm: null");
+  DN_CHECK(((uintptr_t)x | (uintptr_t)gamma | (uintptr_t)beta) % 16 == 0 && (uintptr_t)y % (4 * sizeof(T)) == 0,
+           "layernorm: x, gamma and beta must be 16-byte aligned, y aligned to 4 elements");
   hipLaunchKernelGGL(ln_kernel<T>, dim3(static_cast<unsigned>((M + 3) / 4)), dim3(256), 0, s, x, y, M, C, gamma,
                      beta, eps);
   DN_HIP(hipGetLastError());
