@@ -127,7 +127,8 @@ def _vt_layout(v, heads, dp, ld):
 
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("B,heads,Sq,Skv,d", [(2, 3, 200, 77, 64), (1, 2, 256, 300, 64), (2, 2, 130, 96, 40),
-                                              (2, 4, 256, 256, 16), (1, 1, 5, 1, 64), (2, 20, 1024, 1024, 64)])
+                                              (2, 4, 256, 256, 16), (1, 1, 5, 1, 64), (2, 20, 1024, 1024, 64),
+                                              (1, 3, 2100, 333, 64), (2, 1, 70, 257, 64)])
 def test_attention(dtype, B, heads, Sq, Skv, d):
     announce(f"attention dtype={dtype} B={B} heads={heads} Sq={Sq} Skv={Skv} d={d}")
     r = _rng(B * heads + Sq + Skv + d)
