@@ -50,14 +50,15 @@ template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
 
-__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+// x * sigmoid(x) with the hardware reciprocal (about 1 ulp; no IEEE division sequence).
+__device__ __forceinline__ float silu_f(float x) { return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 
 // Exact-form GELU, x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf from
 // Abramowitz & Stegun (1964) formula 7.1.26: |error| <= 1.5e-7 on the real line
-// (one reciprocal, one exponential, five FMAs instead of a library erf).
+// (one hardware reciprocal, one exponential, five FMAs instead of a library erf).
 __device__ __forceinline__ float gelu_erf(float x) {
   const float z = fabsf(x) * 0.70710678118654752f;
-  const float t = __frcp_rn(1.0f + 0.3275911f * z);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * z);
   const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
   const float e = 1.0f - poly * __expf(-z * z);  // erf(|x| / sqrt 2)
   return 0.5f * x * (1.0f + copysignf(e, x));
