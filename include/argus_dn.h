@@ -199,14 +199,33 @@ dn_status ac_fetch_latent(const uint16_t* cache_latents, int64_t n, int64_t nume
 
 /* ---------------------------------------------------------------------------
  * Single-kernel entry points. They run exactly the kernels dn_denoise runs and
- * exist for element-wise checks at full size and for timing one kernel.
+ * exist for element-wise checks at full size and for timing one kernel. A GEMM
+ * whose tile plan splits K also runs the split-K reduction kernel; its partial
+ * sums live in a per-device workspace the library allocates on first need and
+ * keeps, so calls on one device must not overlap.
  * All buffers are device memory, row-major, in the element type `dtype`
  * (DN_BF16 -> bf16 bits, DN_FP32 -> fp32) unless stated otherwise.
  * ------------------------------------------------------------------------- */
 
+/* Weight layout of the GEMM entry points below. A weight matrix w[N][K] (row n =
+ * output column n; for the 3x3 convolution K = 9 * Cin, tap-major) is passed in
+ * the library's packed layout, which depends only on (dtype, N, K): bf16 matrices
+ * with N % 32 == 0 and K % 64 == 0 are stored in MFMA fragment order (for each
+ * block of 32 rows and each 16 columns, the 64 16-byte operands of one matrix-core
+ * instruction lie in 1 KB of contiguous memory); every other matrix, and every fp32
+ * matrix, is row-major unchanged.
+ * dn_packed_weight_elems: *elems = elements the packed matrix occupies (N rounded
+ *   up to 32, times K, for the fragment order; N * K otherwise).
+ * dn_pack_weight: packs a row-major device matrix w [N][K] (dtype elements) into
+ *   `out` (device, dn_packed_weight_elems elements, not overlapping w). K must be a
+ *   multiple of 16. Asynchronous on `stream`. */
+dn_status dn_packed_weight_elems(int32_t dtype, int32_t N, int32_t K, int64_t* elems);
+dn_status dn_pack_weight(int32_t dtype, const void* w, int32_t N, int32_t K, void* out, void* stream);
+
 /* Dense layer (the transformer's projections and feed-forward):
  * y[m][n] = sum_k x[m][k] * w[n][k] + bias[n] (+ resid[m][n]).
- * x [M][K], w [N][K], bias fp32 [N] or NULL, resid [M][N] or NULL, y [M][N].
+ * x [M][K], w [N][K] packed by dn_pack_weight, bias fp32 [N] or NULL, resid
+ * [M][N] or NULL, y [M][N].
  * K must be a multiple of 64 (bf16) / 32 (fp32). Output fp32 when y_f32 != 0,
  * else `dtype`; resid fp32 when resid_f32 != 0, else `dtype`.
  * geglu != 0 (GEGLU feed-forward, Shazeer 2020): w has 2N rows and bias 2N
@@ -221,7 +240,8 @@ dn_status dn_op_linear(int32_t dtype, const void* x, const void* w, const float*
 /* 3x3 convolution (cross-correlation, zero padding 1, bias) as an implicit GEMM
  * on NHWC activations: x [n][H][W][Cin]; with up = 1 the input is first
  * nearest-neighbour upsampled to 2H x 2W (never materialised); stride 1 or 2.
- * w [Cout][3][3][Cin] (tap-major: PyTorch [Cout][Cin][3][3] permuted), bias fp32
+ * w [Cout][3][3][Cin] (tap-major: PyTorch [Cout][Cin][3][3] permuted; packed by
+ * dn_pack_weight as an N = Cout, K = 9 * Cin matrix), bias fp32
  * [Cout] or NULL, temb fp32 [n][Cout] or NULL (added per sample, as a ResBlock
  * adds its time-embedding projection), resid [n][Ho][Wo][Cout] or NULL,
  * y [n][Ho][Wo][Cout] with Ho = (Hl - 1) / stride + 1 for the logical input
@@ -248,7 +268,8 @@ dn_status dn_op_attention(int32_t dtype, const void* q, int32_t ldq, const void*
  * acc[m][n] = sum_k x[m][k] * w[n][k] + bias[n] for n < N; columns n < vt_col0
  * go to y [M][vt_col0] (e.g. Q and K), columns n >= vt_col0 (heads * head_stride
  * of them) go to vt [M / seq][heads][head_stride][vt_ld] at token m % seq.
- * Same kernels and tile plan as dn_op_linear. Asynchronous. */
+ * w packed by dn_pack_weight. Same kernels and tile plan as dn_op_linear.
+ * Asynchronous. */
 dn_status dn_op_linear_vt(int32_t dtype, const void* x, const void* w, const float* bias, void* y, int64_t M,
                           int32_t N, int32_t K, int32_t vt_col0, void* vt, int32_t heads, int32_t head_stride,
                           int32_t seq, int32_t vt_ld, void* stream);

@@ -56,6 +56,8 @@ bool is_dtype(int32_t d) { return d == DN_FP32 || d == DN_BF16; }
 struct OpDev {
   int cus = 0;
   void* zero = nullptr;
+  float* part = nullptr;  // split-K partial slabs, grown on demand
+  size_t part_floats = 0;
 };
 std::mutex g_op_mu;
 std::vector<OpDev> g_op_dev;
@@ -75,10 +77,24 @@ template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
       DN_HIP(hipMemset(d.zero, 0, 256));
       d.cus = prop.multiProcessorCount;
     }
+    const dn::GemmPlan g0 = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, d.cus, p.vt == nullptr);
+    const size_t need = dn::gemm_workspace_floats(g0, p.M, p.N);
+    if (need > d.part_floats) {
+      if (d.part) {
+        DN_HIP(hipDeviceSynchronize());
+        DN_HIP(hipFree(d.part));
+        d.part = nullptr;
+        d.part_floats = 0;
+      }
+      DN_HIP(hipMalloc(&d.part, need * 4));
+      d.part_floats = need;
+    }
     w = d;
   }
-  const dn::GemmPlan g = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, w.cus);
+  const dn::GemmPlan g = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, w.cus, p.vt == nullptr);
   p.zero16 = w.zero;
+  p.part = w.part;
+  p.part_floats = w.part_floats;
   dn::gemm<T>(p, g, s);
 }
 
@@ -175,6 +191,29 @@ dn_status ac_fetch_latent(const uint16_t* cache_latents, int64_t n, int64_t nume
     DN_CHECK(n >= 1 && numel >= 1, "ac_fetch_latent: empty cache");
     DN_CHECK(idx >= 0 && idx < n, "ac_fetch_latent: index out of range");
     dn::bf16_latent_to_f32(cache_latents + idx * numel, latent, numel, as_stream(stream));
+  });
+}
+
+dn_status dn_packed_weight_elems(int32_t dtype, int32_t N, int32_t K, int64_t* elems) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_packed_weight_elems: bad dtype");
+    DN_CHECK(elems, "dn_packed_weight_elems: null pointer");
+    DN_CHECK(N >= 1 && K >= 1, "dn_packed_weight_elems: bad sizes");
+    *elems = dtype == DN_BF16 && dn::gemm_frag_layout(N, K) ? (int64_t)dn::gemm_frag_elems(N, K) : (int64_t)N * K;
+  });
+}
+
+dn_status dn_pack_weight(int32_t dtype, const void* w, int32_t N, int32_t K, void* out, void* stream) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_pack_weight: bad dtype");
+    DN_CHECK(w && out, "dn_pack_weight: null pointer");
+    DN_CHECK(N >= 1 && K >= 1 && K % 16 == 0, "dn_pack_weight: bad sizes (K must be a multiple of 16)");
+    if (dtype == DN_BF16 && dn::gemm_frag_layout(N, K)) {
+      dn::to_frag(static_cast<const dn::bf16*>(w), N, K, K, static_cast<dn::bf16*>(out), as_stream(stream));
+    } else {
+      const size_t bytes = (size_t)N * K * (dtype == DN_BF16 ? 2 : 4);
+      DN_HIP(hipMemcpyAsync(out, w, bytes, hipMemcpyDeviceToDevice, as_stream(stream)));
+    }
   });
 }
 

@@ -18,6 +18,8 @@
 // Work distribution: tiles are numbered so that each XCD (consecutive
 // workgroup ids go round-robin over the 8 XCDs) works through a contiguous band
 // of output columns with all row tiles, keeping that band of B in its L2.
+#include <algorithm>
+
 #include "gemm_epilogue.h"
 
 namespace dn {
@@ -262,7 +264,48 @@ template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPl
 //    128 x 128 tiles with two resident workgroups per CU;
 //  - fp32 (the check mode), narrow outputs (N < 128) and K not a multiple of 64 take
 //    the register-staged kernel.
-template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus) {
+// Fragment-B kernel (bf16 weights in fragment order). Three tile variants share a CU
+// between several workgroups: 128 x 256 (two per CU), 128 x 128 (two) and 64 x 128
+// (four). The plan minimises a cost model fitted to measured SD-XL GEMM times on MI355X
+// (bf16, weights streamed from HBM): a run takes ceil(units / slots) rounds, a round
+// costs the MFMA work of the units resident on a CU at a per-CU rate R plus a fixed
+// prologue / epilogue cost O, and a K split adds the fp32 slabs written and read by the
+// reduction. GEGLU needs 64-column value/gate pairs per wave (the 128 x 256 tile).
+GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split) {
+  struct Var {
+    int bm, bn, wg;
+    double rate, fixed;  // FLOP per us per CU, us per round
+  };
+  static const Var vars[] = {{128, 256, 2, 2.4e6, 8.0}, {128, 128, 2, 2.0e6, 5.0}, {64, 128, 4, 2.0e6, 2.0}};
+  GemmPlan best{128, 256, 0};
+  best.stages = 3;
+  best.frag = 1;
+  double best_t = 1e300;
+  const int nk = K / 64;
+  for (const Var& v : vars) {
+    if (geglu && v.bn != 256) continue;
+    const long long tiles = (long long)ceil_div(M, v.bm) * ceil_div(N, v.bn);
+    for (int sp = 1; sp <= kMaxSplit; ++sp) {
+      if (sp > 1 && (geglu || !allow_split || nk / sp < 4)) break;
+      const long long units = tiles * sp;
+      const long long slots = (long long)cus * v.wg;
+      const long long rounds = (units + slots - 1) / slots;
+      const double per_cu = std::max(1.0, (double)std::min(units, slots) / cus);
+      double t = rounds * (per_cu * 2.0 * v.bm * v.bn * ((double)K / sp) / v.rate + v.fixed);
+      if (sp > 1) t += 0.2 * (sp + 1.0) * M * N * 4.0 / 1e6 + 2.0;
+      if (t < best_t) {
+        best_t = t;
+        best.bm = v.bm;
+        best.bn = v.bn;
+        best.split = sp;
+      }
+    }
+  }
+  return best;
+}
+
+template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split) {
+  if (sizeof(T) == 2 && gemm_frag_layout(N, K)) return frag_plan(M, N, K, geglu, cus, allow_split);
   const long long t128 = (long long)ceil_div(M, 128) * ceil_div(N, 128);
   if (sizeof(T) == 2 && N >= 128 && K % 64 == 0 && M >= 8192) {
     const long long t256 = (long long)ceil_div(M, 256) * ceil_div(N, 256);
@@ -288,6 +331,11 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
   DN_CHECK(p.ldb % (16 / (int)sizeof(T)) == 0 && p.lda0 % (16 / (int)sizeof(T)) == 0 &&
                (p.c1 == 0 || p.lda1 % (16 / (int)sizeof(T)) == 0),
            "gemm: leading dimensions must be multiples of 16 bytes");
+  if (g.frag) {
+    DN_CHECK(sizeof(T) == 2, "gemm: the fragment-B kernel is bf16 only");
+    gemm_bf16_frag(p, g, s);
+    return;
+  }
   if (g.dma) {
     DN_CHECK(sizeof(T) == 2, "gemm: the direct-to-LDS kernel is bf16 only");
     gemm_bf16_dma(p, g, s);
@@ -299,8 +347,8 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
     dispatch<T, false>(p, g, s);
 }
 
-template GemmPlan gemm_plan<float>(int, int, int, int, int);
-template GemmPlan gemm_plan<bf16>(int, int, int, int, int);
+template GemmPlan gemm_plan<float>(int, int, int, int, int, bool);
+template GemmPlan gemm_plan<bf16>(int, int, int, int, int, bool);
 template void gemm<float>(const GemmParams&, const GemmPlan&, hipStream_t);
 template void gemm<bf16>(const GemmParams&, const GemmPlan&, hipStream_t);
 

@@ -1,0 +1,495 @@
+// bf16 GEMM / implicit-GEMM conv with fragment-ordered weights (gfx950).
+//
+// Same contraction and epilogue as gemm.hip (see kernels.h), organised for the
+// dense bf16 hot path:
+//  - B, the packed weight matrix, is stored in MFMA fragment order (gemm_frag_index):
+//    for each block of 32 output columns and each k-step of 16, the 64 lanes' 16-byte
+//    operands lie in 1 KB of contiguous memory. Each wave loads its own B fragments
+//    with one coalesced 16-byte load per lane straight into registers, two LDS stages
+//    ahead, so B costs no LDS bandwidth;
+//  - A (the activations, or the implicit-convolution gather) goes global -> LDS with
+//    global_load_lds_dwordx4 into S stages of BK = 64 (128-byte rows, chunk c of row r
+//    at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1)), shared by the 4 waves;
+//  - block tile BM x 4 * 32 FN: the 4 waves split the columns, each computes BM x 32 FN
+//    with 32x32x16 MFMAs issued as C^T = B A^T (four consecutive output columns per lane);
+//  - every k-step interleaves one MFMA, one LDS fragment read for the next k-step and
+//    its share of B loads (scheduling groups); the stage hand-over (wait + barrier)
+//    sits before the last k-step, whose MFMAs cover the first reads of the next stage;
+//  - split-K: the units (tile, split) cover contiguous K ranges and write fp32 partial
+//    tiles; a second kernel sums the slabs in split order (deterministic) and applies
+//    the epilogue;
+//  - epilogue through LDS: each wave writes its accumulators to LDS and reads them back
+//    row-contiguous, so bias / residual loads and output stores are whole row segments
+//    of 64-256 bytes instead of 16-byte pieces of 32 different rows. The per-head V^T
+//    columns keep the register layout, where consecutive lanes are consecutive tokens.
+//  - tiles go to XCDs in contiguous ranges (workgroup ids are dealt round-robin over the
+//    8 XCDs), ordered by column band, split, then row tile, so that the units sharing a
+//    band of B run on one XCD and share its L2.
+#include <algorithm>
+#include <type_traits>
+
+#include "gemm_epilogue.h"
+
+namespace dn {
+namespace {
+
+constexpr int kXcds = 8;
+constexpr int kBK = 64;
+constexpr int kRowBytes = 128;
+constexpr int kThreads = 256;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void gbl_void;
+
+// s_waitcnt immediate: vmcnt <= vm (bits 3:0 and 15:14), lgkmcnt <= 0 (bits 11:8),
+// expcnt unconstrained (bits 6:4 = 7).
+constexpr int wait_vm_lgkm0(int vm) { return (vm & 0xF) | (((vm >> 4) & 3) << 14) | (7 << 4); }
+
+// Scheduling-group pattern of one k-step: NM MFMAs, each followed by one LDS read
+// (while the NR reads last) and by its share of the NV B loads.
+template <int I, int NM, int NR, int NV> struct KSched {
+  __device__ static __forceinline__ void apply() {
+    if constexpr (I < NM) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      if constexpr (I < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      constexpr int v = NV * (I + 1) / NM - NV * I / NM;
+      if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);  // VM load
+      KSched<I + 1, NM, NR, NV>::apply();
+    }
+  }
+};
+
+template <int BM, int FN, int S> constexpr size_t frag_lds_bytes() {
+  constexpr size_t stages = size_t(S) * BM * kRowBytes;
+  constexpr size_t epi = size_t(4) * 32 * (32 * FN + 4) * 4;
+  return stages > epi ? stages : epi;
+}
+
+// MODE: 0 linear layer (one A source), 1 linear layer over two concatenated A sources,
+// 2 implicit 3x3 convolution (one source). SPLIT: write fp32 partial tiles.
+// D: B register buffers (B is loaded D stages ahead). WPE: waves per SIMD the register
+// allocation must allow (2: two workgroups share a CU, so one's prologue, barriers and
+// epilogue overlap the other's MFMAs).
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_frag_kernel(
+    GemmParams p, int mt, int nt, int nsplit) {
+  constexpr int FM = BM / 32;
+  constexpr int WN = 32 * FN;
+  constexpr int BN = 4 * WN;
+  constexpr int STAGE = BM * kRowBytes;
+  constexpr int PW = BM / 32;  // DMA instructions (8 rows of 128 B) per wave per stage
+  constexpr int NM = FM * FN;
+  static_assert(D == 1 || D == 2, "one or two B buffers");
+  // S <= 3: the hand-over wait below also covers the prologue stages only up to S = 3
+  static_assert(S >= 2 && S <= 3, "2 or 3 LDS stages");
+  static_assert(BM % 32 == 0 && BM <= 256, "BM");
+
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  // ---- unit assignment (see the file comment)
+  const int units = mt * nt * nsplit;
+  const int wg = blockIdx.x;
+  const int xcd = wg % kXcds, idx = wg / kXcds;
+  const int base = units / kXcds, rem = units % kXcds;
+  const int logical = xcd * base + min(xcd, rem) + idx;
+  const int m_tile = logical % mt;
+  const int ns = logical / mt;
+  const int split = ns % nsplit;
+  const int n_tile = ns / nsplit;
+  const int n0 = n_tile * BN, m0 = m_tile * BM;
+  const int nk = p.K / kBK;
+  const int kt0 = (int)((long long)split * nk / nsplit);
+  const int kt1 = (int)((long long)(split + 1) * nk / nsplit);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+  // ---- A rows: instruction j of this wave loads tile rows [8 q, 8 q + 8), q = wave * PW + j;
+  // the lane fetches logical chunk (lane & 7) ^ f(row) of row 8 q + (lane >> 3). Each row
+  // keeps a 32-bit element offset at k = 0 (linear: row * lda; conv: the input pixel of tap
+  // (0, 0), possibly outside the image, times lda) and, for conv, a tap mask (bit 3 ky + kx:
+  // tap inside the input; bits 9 / 10: output row / column parity, which picks the source
+  // pixel of the taps of a nearest-x2 upsampled input); MODE 1 keeps the second source's
+  // offset instead.
+  const int lrow = lane >> 3;
+  const int lc_even = ((lane & 7) ^ lrow) * 8, lc_odd = ((lane & 7) ^ lrow ^ 1) * 8;
+  int off0[PW];
+  int off1[PW];
+  const int hl = p.in_h << p.up, wl = p.in_w << p.up;
+#pragma unroll
+  for (int j = 0; j < PW; ++j) {
+    const int q = wave * PW + j;
+    const int lc = (q & 1) ? lc_odd : lc_even;
+    const int m = min(m0 + 8 * q + lrow, p.M - 1);
+    off1[j] = 0;
+    if (MODE == 2) {
+      const int opix = p.out_h * p.out_w;
+      const int smp = m / opix;
+      const int r2 = m - smp * opix;
+      const int oy = r2 / p.out_w, ox = r2 - (r2 / p.out_w) * p.out_w;
+      const int iy0 = oy * p.stride - 1, ix0 = ox * p.stride - 1;
+      int mk = 0;
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int iy = iy0 + t / 3, ix = ix0 + t % 3;
+        mk |= (iy >= 0 && iy < hl && ix >= 0 && ix < wl) ? (1 << t) : 0;
+      }
+      mk |= (oy & 1) << 9 | (ox & 1) << 10;
+      const int pix = (smp * p.in_h + (iy0 >> p.up)) * p.in_w + (ix0 >> p.up);
+      off0[j] = pix * p.lda0 + lc;
+      off1[j] = mk;
+    } else {
+      off0[j] = m * p.lda0 + lc;
+      if (MODE == 1) off1[j] = m * p.lda1 + lc;
+    }
+  }
+  const int ct = p.c0 + p.c1;
+  const bf16* const gA0 = static_cast<const bf16*>(p.a0);
+  const bf16* const gA1 = static_cast<const bf16*>(p.a1);
+
+  // DMA of A stage kt into LDS slot `slot`: PW global_load_lds per wave, no branches.
+  // Stages past this unit's range read the 16-byte zero block instead, so every
+  // hand-over issues the same number of loads.
+  auto issue_a = [&](int kt_in, int slot) {
+    const bool real = kt_in < kt1;
+    const int kt = real ? kt_in : kt1 - 1;
+    const int k0 = kt * kBK;
+    unsigned char* stage = smem + slot * STAGE;
+    int tap = 0, c = k0;
+    if (MODE == 2) {
+      tap = k0 / ct;
+      c = k0 - tap * ct;
+    }
+    const int ky = tap / 3, kx = tap - 3 * (tap / 3);
+    const bool second = MODE == 1 && c >= p.c0;
+    const bf16* a_src = second ? gA1 : gA0;
+    const int a_c = second ? c - p.c0 : c;
+    const int tap_off = (MODE == 2 && !p.up) ? (ky * p.in_w + kx) * p.lda0 : 0;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int q = wave * PW + j;
+      const bf16* g;
+      if (MODE == 2) {
+        int off = off0[j] + a_c + tap_off;
+        if (p.up) {
+          const int dy = ky == 2 || (ky == 1 && !(off1[j] & (1 << 9)));
+          const int dx = kx == 2 || (kx == 1 && !(off1[j] & (1 << 10)));
+          off += (dy ? p.in_w * p.lda0 : 0) + (dx ? p.lda0 : 0);
+        }
+        const bool inb = (off1[j] >> tap) & 1;
+        g = inb ? a_src + off : static_cast<const bf16*>(p.zero16);
+      } else {
+        g = a_src + ((MODE == 1 && second) ? off1[j] : off0[j]) + a_c;
+      }
+      if (!real) g = static_cast<const bf16*>(p.zero16);
+      __builtin_amdgcn_global_load_lds((gbl_void*)g, (lds_void*)(stage + q * 1024), 16, 0, 0);
+    }
+  };
+
+  // ---- B fragments of this wave: column blocks nb = (n0 + wave * WN) / 32 + j, clamped
+  // to the packed rows (columns past N are computed and dropped by the epilogue).
+  const int kbs = p.K / 16;
+  const int nb_last = (p.N + 31) / 32 - 1;
+  const bf16* bptr[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int nb = min((n0 + wave * WN) / 32 + j, nb_last);
+    bptr[j] = static_cast<const bf16*>(p.b) + (long long)nb * kbs * 512 + lane * 8;
+  }
+  typedef bf16x8 BReg[4][FN];
+  auto load_b_step = [&](int kt_in, int s, BReg& dst) {
+    const int kt = kt_in < kt1 ? kt_in : kt1 - 1;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) dst[s][j] = *reinterpret_cast<const bf16x8*>(bptr[j] + (kt * 4 + s) * 512);
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // A fragment of k-step s: row (lane % 32) of each 32-row block, logical chunk
+  // 2 s + (lane / 32) at its swizzled position.
+  const int frow = lane & 31;
+  const int fs = (lane & 7) ^ ((lane >> 3) & 1);
+  const int hh = lane >> 5;
+  bf16x8 fa[2][FM];
+  auto read_a = [&](int slot, int s, bf16x8* a) {
+    const unsigned char* st = smem + slot * STAGE + frow * kRowBytes + (((2 * s + hh) ^ fs) * 16);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) a[i] = *reinterpret_cast<const bf16x8*>(st + i * 32 * kRowBytes);
+  };
+  auto mfmas = [&](const bf16x8* a, const bf16x8* b) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
+  };
+
+  BReg bq[D];
+  // One k-step: [the DMA of a later A stage first, when `dma`], the next k-step's A
+  // fragments from LDS, this k-step's MFMAs and the B loads of stage kt + D for this
+  // k-step, interleaved one MFMA / one LDS read / a share of the VM loads.
+  auto kstep = [&](auto dma, int dma_kt, int dma_slot, int rd_slot, int rd_s, bf16x8* a_use, bf16x8* a_next,
+                   bf16x8* b_use, int bkt, int s, BReg& bb) {
+    if constexpr (decltype(dma)::value) issue_a(dma_kt, dma_slot);
+    read_a(rd_slot, rd_s, a_next);
+    mfmas(a_use, b_use);
+    load_b_step(bkt, s, bb);
+    if constexpr (decltype(dma)::value) __builtin_amdgcn_sched_group_barrier(0x020, PW, 0);
+    KSched<0, NM, FM, FN>::apply();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // prologue: A stages kt0 .. kt0 + S - 1 (every slot), B stages kt0 .. kt0 + D - 1; the
+  // wait covers A stages kt0 and kt0 + 1 (so the first hand-over needs no count of its own)
+#pragma unroll
+  for (int s = 0; s < S; ++s) issue_a(kt0 + s, s);
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) load_b_step(kt0 + d, s, bq[d]);
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((S - 2) * PW + D * 4 * FN));
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  read_a(0, 0, fa[0]);
+
+  // Stage kt (slot (kt - kt0) % S, B buffer bb): k-steps 0..2; the hand-over: this wave's
+  // DMA of stage kt + 1 has landed once at most VM_END later VM loads are pending, and
+  // after the barrier every wave's has, and every wave is done reading slot kt; then
+  // k-step 3 issues stage kt + S into that slot and reads stage kt + 1's first fragments.
+  // VM loads issued after the DMA of stage kt + 1 (made in k-step 3 of stage kt + 1 - S):
+  // B(3) of that stage, S - 2 whole stages (4 FN B loads + PW DMA each), B(0..2) of stage kt.
+  // Stage kt0 + 1 was waited for in the prologue; the DMA of stage kt0 + 2 (S = 3, in the
+  // prologue) is followed by D * 4 FN + 4 FN + PW + 3 FN >= VM_END loads.
+  constexpr int VM_END = 4 * FN + (S - 2) * (4 * FN + PW);
+  static_assert(VM_END < 64 && (S - 2) * PW + D * 4 * FN < 64, "vmcnt range");
+  auto stage = [&](int kt, BReg& bb) {
+    const int rel = kt - kt0;
+    const int slot = rel % S;
+    const int nslot = (rel + 1) % S;
+    kstep(std::false_type{}, 0, 0, slot, 1, fa[0], fa[1], bb[0], kt + D, 0, bb);
+    kstep(std::false_type{}, 0, 0, slot, 2, fa[1], fa[0], bb[1], kt + D, 1, bb);
+    kstep(std::false_type{}, 0, 0, slot, 3, fa[0], fa[1], bb[2], kt + D, 2, bb);
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(VM_END));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    kstep(std::true_type{}, kt + S, slot, nslot, 0, fa[1], fa[0], bb[3], kt + D, 3, bb);
+  };
+
+  if constexpr (D == 2) {
+    for (int kt = kt0; kt < kt1; kt += 2) {
+      stage(kt, bq[0]);
+      if (kt + 1 < kt1) stage(kt + 1, bq[D - 1]);
+    }
+  } else {
+    for (int kt = kt0; kt < kt1; ++kt) stage(kt, bq[0]);
+  }
+  // The loads past the range (zero block, clamped B) must land before LDS is reused.
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+  __syncthreads();
+
+  // ---- epilogue
+  const int col = lane & 31;
+  const int h4 = 4 * (lane >> 5);
+  const int nw0 = n0 + wave * WN;
+  if (!SPLIT && p.vt && nw0 + WN > p.vt_col0) {
+    // columns of the per-head V^T output (or a wave straddling it): register layout,
+    // lanes 0..31 = 32 consecutive tokens of one column
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int m = m0 + i * 32 + col;
+      if (m >= p.M) continue;
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nw0 + j * 32 + 8 * g + h4;
+          float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+          epilogue_group<bf16>(p, m, n, v);
+        }
+    }
+    return;
+  }
+  // Row-contiguous phase: 32 rows x WN fp32 per wave in LDS (row pitch WN + 4 floats:
+  // the 16-byte writes of rows r .. r + 7 fall on distinct banks).
+  constexpr int EPL = WN + 4;
+  float* ep = reinterpret_cast<float*>(smem) + wave * (32 * EPL);
+  float* slab = SPLIT ? p.part + (long long)split * p.M * p.n_store : nullptr;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(ep + col * EPL + j * 32 + 8 * g + h4) =
+            f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+    const int mb = m0 + i * 32;
+    if (SPLIT || !p.geglu) {
+      constexpr int LPR = WN / 4;   // lanes per row
+      constexpr int RPI = 64 / LPR; // rows per pass
+#pragma unroll
+      for (int t = 0; t < 32 / RPI; ++t) {
+        const int rr = t * RPI + lane / LPR;
+        const int c4 = (lane % LPR) * 4;
+        const f32x4 v4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c4);
+        const int m = mb + rr, n = nw0 + c4;
+        if (m >= p.M || n >= p.n_store) continue;
+        if (SPLIT) {
+          *reinterpret_cast<f32x4*>(slab + (long long)m * p.n_store + n) = v4;
+        } else {
+          float v[4] = {v4[0], v4[1], v4[2], v4[3]};
+          epilogue_group<bf16>(p, m, n, v);
+        }
+      }
+    } else {
+      // GEGLU: within each 64-column pair block, columns [0, 32) are values and
+      // [32, 64) the matching gates; output column = (pair block) * 32 + c
+      constexpr int LPR = WN / 8;
+      constexpr int RPI = 64 / LPR;
+#pragma unroll
+      for (int t = 0; t < 32 / RPI; ++t) {
+        const int rr = t * RPI + lane / LPR;
+        const int cq = (lane % LPR) * 4;            // 0 .. WN/2 - 4
+        const int pb = cq / 32, c4 = cq % 32;       // pair block, column in it
+        const int lc = pb * 64 + c4;                // value column within the wave
+        const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc);
+        const f32x4 g4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 32);
+        const int m = mb + rr;
+        const int nv = nw0 + lc;
+        const int o = nw0 / 2 + cq;
+        if (m >= p.M || o >= p.n_store) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float a = a4[e] + (p.bias ? p.bias[nv + e] : 0.f);
+          const float gg = g4[e] + (p.bias ? p.bias[nv + 32 + e] : 0.f);
+          v[e] = a * gelu_erf(gg);
+        }
+        store4<bf16>(p, m, o, v, p.n_store);
+      }
+    }
+  }
+}
+
+// Sum of the split-K partial slabs [nsplit][M][n_store] in split order, then the
+// epilogue; one thread per 4 consecutive columns of a row.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, int nsplit) {
+  const int q = p.n_store / 4;
+  const long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  if (i >= (long long)p.M * q) return;
+  const int m = (int)(i / q);
+  const int n = (int)(i - (long long)m * q) * 4;
+  const long long slab = (long long)p.M * p.n_store;
+  const float* src = p.part + (long long)m * p.n_store + n;
+  f32x4 s = *reinterpret_cast<const f32x4*>(src);
+  for (int k = 1; k < nsplit; ++k) {
+    const f32x4 t = *reinterpret_cast<const f32x4*>(src + k * slab);
+    s[0] += t[0];
+    s[1] += t[1];
+    s[2] += t[2];
+    s[3] += t[3];
+  }
+  float v[4] = {s[0], s[1], s[2], s[3]};
+  epilogue_group<bf16>(p, m, n, v);
+}
+
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT>
+void launch_frag(const GemmParams& p, int nsplit, hipStream_t s) {
+  constexpr size_t lds = frag_lds_bytes<BM, FN, S>();
+  static bool attr_set = false;
+  if (!attr_set) {
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+    attr_set = true;
+  }
+  const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, 128 * FN);
+  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT>), dim3(mt * nt * nsplit), dim3(kThreads), lds,
+                     s, p, mt, nt, nsplit);
+  DN_HIP(hipGetLastError());
+}
+
+template <int BM, int FN, int S, int D, int WPE, int MODE>
+void run_frag(const GemmParams& p, int nsplit, hipStream_t s) {
+  if (nsplit > 1) {
+    launch_frag<BM, FN, S, D, WPE, MODE, true>(p, nsplit, s);
+    const long long nq = (long long)p.M * (p.n_store / 4);
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, p,
+                       nsplit);
+    DN_HIP(hipGetLastError());
+  } else {
+    launch_frag<BM, FN, S, D, WPE, MODE, false>(p, 1, s);
+  }
+}
+
+// Tile plans (three LDS stages): 128 x 256 (FN = 2) with one B buffer, two workgroups per
+// CU; 128 x 128 (FN = 1) and 64 x 128 with two B buffers, two / four workgroups per CU.
+// stages = 2 selects the 128 x 256 variant with two B buffers and one workgroup per CU.
+template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
+  if (g.bm == 128 && g.bn == 256 && g.stages == 3) return run_frag<128, 2, 3, 1, 2, MODE>(p, g.split, s);
+  if (g.bm == 128 && g.bn == 256 && g.stages == 2) return run_frag<128, 2, 3, 2, 1, MODE>(p, g.split, s);
+  if (g.bm == 128 && g.bn == 128 && g.stages == 3) return run_frag<128, 1, 3, 2, 2, MODE>(p, g.split, s);
+  if (g.bm == 64 && g.bn == 128 && g.stages == 3) return run_frag<64, 1, 3, 2, 4, MODE>(p, g.split, s);
+  throw Error(-1, "gemm: no fragment-B kernel for this tile plan");
+}
+
+// Fragment order of a packed [N][K] weight matrix (N rounded up to 32, K % 16 == 0):
+// element (n, k) lives at ((n / 32) * (K / 16) + k / 16) * 512 + lane * 8 + k % 8 with
+// lane = n % 32 + 32 * ((k % 16) / 8).
+__global__ void to_frag_kernel(const bf16* src, int N, int K, int lds, bf16* dst, int Npad) {
+  const long long nv = (long long)Npad * K / 8;
+  const int kbs = K / 16;
+  for (long long v = blockIdx.x * (long long)blockDim.x + threadIdx.x; v < nv; v += (long long)gridDim.x * blockDim.x) {
+    const int lane = (int)(v % 64);
+    const long long t = v / 64;
+    const int kb = (int)(t % kbs);
+    const int nb = (int)(t / kbs);
+    const int n = nb * 32 + (lane & 31);
+    const int k = kb * 16 + (lane >> 5) * 8;
+    uint4 val = make_uint4(0u, 0u, 0u, 0u);
+    if (n < N) val = *reinterpret_cast<const uint4*>(src + (long long)n * lds + k);
+    *reinterpret_cast<uint4*>(dst + v * 8) = val;
+  }
+}
+
+}  // namespace
+
+bool gemm_frag_layout(int N, int K) { return N >= 32 && N % 32 == 0 && K >= kBK && K % kBK == 0; }
+
+size_t gemm_frag_elems(int N, int K) { return (size_t)((N + 31) / 32 * 32) * K; }
+
+void to_frag(const bf16* src, int N, int K, int ld_src, bf16* dst, hipStream_t s) {
+  DN_CHECK(K % 16 == 0 && ld_src % 8 == 0 && ld_src >= K, "to_frag: K and the source pitch must suit 16-byte rows");
+  const int Npad = (N + 31) / 32 * 32;
+  const long long nv = (long long)Npad * K / 8;
+  const int blocks = static_cast<int>(std::min<long long>((nv + 255) / 256, 16384));
+  hipLaunchKernelGGL(to_frag_kernel, dim3(std::max(blocks, 1)), dim3(256), 0, s, src, N, K, ld_src, dst, Npad);
+  DN_HIP(hipGetLastError());
+}
+
+void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
+  DN_CHECK(gemm_frag_layout(p.N, p.K), "gemm: fragment-B kernel needs N % 32 == 0 and K % 64 == 0");
+  DN_CHECK(p.taps == 1 || (p.c0 + p.c1) % kBK == 0, "gemm: conv channels must be a multiple of 64");
+  DN_CHECK(p.c1 == 0 || p.c0 % kBK == 0, "gemm: concatenation split must be a multiple of 64");
+  DN_CHECK(p.taps == 1 || p.zero16, "gemm: implicit conv needs the zero block");
+  DN_CHECK(p.taps == 1 || p.c1 == 0, "gemm: the fragment-B conv takes one input source");
+  DN_CHECK(g.split >= 1 && g.split <= kMaxSplit && p.K / kBK >= g.split, "gemm: bad split");
+  DN_CHECK(!p.geglu || (g.bn / 4) % 64 == 0, "gemm: GEGLU needs 64-column value/gate pairs per wave");
+  if (g.split > 1) {
+    DN_CHECK(!p.geglu && !p.vt, "gemm: split-K takes neither GEGLU nor the V^T output");
+    DN_CHECK(p.n_store % 4 == 0 && p.n_store == p.N, "gemm: split-K needs n_store == N, a multiple of 4");
+    DN_CHECK(p.part && p.part_floats >= (size_t)g.split * p.M * p.n_store, "gemm: split-K workspace too small");
+  }
+  if (p.taps == 9)
+    dispatch_frag<2>(p, g, s);
+  else if (p.c1)
+    dispatch_frag<1>(p, g, s);
+  else
+    dispatch_frag<0>(p, g, s);
+}
+
+}  // namespace dn

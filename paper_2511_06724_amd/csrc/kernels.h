@@ -43,6 +43,9 @@ struct GemmParams {
   // stride 1 and d stride vt_ld; rows are tokens, vt_seq per sample.
   void* vt = nullptr;
   int vt_col0 = 0, vt_dp = 0, vt_heads = 0, vt_seq = 1, vt_ld = 0;
+  // Split-K workspace (fragment-B kernel): fp32 partial slabs [split][M][n_store].
+  float* part = nullptr;
+  size_t part_floats = 0;
 };
 
 // Block tile (bm x bn) of one GEMM launch and the kernel that runs it.
@@ -50,11 +53,26 @@ struct GemmPlan {
   int bm, bn;
   int dma = 0;  // 1: bf16 direct-to-LDS kernel (gemm_dma.hip), else the register-staged kernel
   int wgm = 2, wgn = 2;  // direct-to-LDS kernel: wave grid over the block tile
-  int stages = 2;        // direct-to-LDS kernel: LDS pipeline depth
+  int stages = 2;        // direct-to-LDS / fragment-B kernels: LDS pipeline depth
+  int frag = 0;          // 1: bf16 fragment-B kernel (gemm_frag.hip)
+  int split = 1;         // fragment-B kernel: K split in this many ranges (fp32 partials + reduce)
 };
-template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus);
+constexpr int kMaxSplit = 8;
+// allow_split = false for epilogues split-K does not support (the per-head V^T output).
+template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split = true);
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 void gemm_bf16_dma(const GemmParams& p, const GemmPlan& g, hipStream_t s);
+void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s);
+// bf16 weight matrices [N][K] with gemm_frag_layout(N, K) are stored in MFMA fragment
+// order (gemm_frag.hip) and multiplied by the fragment-B kernel; every other shape,
+// and fp32, keeps the row-major [N][K] layout.
+bool gemm_frag_layout(int N, int K);
+size_t gemm_frag_elems(int N, int K);  // N rounded up to 32, times K
+void to_frag(const bf16* src, int N, int K, int ld_src, bf16* dst, hipStream_t s);
+// fp32 workspace floats the plan needs (split-K partial slabs), 0 when none.
+inline size_t gemm_workspace_floats(const GemmPlan& g, int M, int N) {
+  return g.frag && g.split > 1 ? (size_t)g.split * M * N : 0;
+}
 template <typename T> constexpr int gemm_bk() { return sizeof(T) == 2 ? 64 : 32; }
 
 // ---------------------------------------------------------------- attention
@@ -128,6 +146,7 @@ struct PackParams {
   int src_rows = 0, src_cols = 0;  // source matrix [src_rows][src_cols]
   int D = 0, Dp = 0;               // head dim and padded head dim
   int Cin = 0, Cinp = 0;           // conv input channels and padded count
+  int frag = 0;                    // 1: write dst in fragment order (gemm_frag.hip; ld_dst unused)
 };
 template <typename T> void pack(const PackParams& p, hipStream_t s);
 void pack_bias(float* dst, int n, const float* src, int src_n, int row_mode, int D, int Dp, hipStream_t s);

@@ -171,7 +171,12 @@ template <typename T> __global__ void pack_kernel(PackParams p) {
         if (ci < p.Cin) v = p.src[(sr * p.Cin + ci) * 9 + tap];
       }
     }
-    static_cast<T*>(p.dst)[(long long)r * p.ld_dst + c] = from_f32<T>(v);
+    long long o = (long long)r * p.ld_dst + c;
+    if (p.frag) {  // fragment order of a [rows][cols] matrix, see gemm_frag.hip
+      const int lane = (r & 31) + 32 * ((c & 15) >> 3);
+      o = ((long long)(r >> 5) * (p.cols >> 4) + (c >> 4)) * 512 + lane * 8 + (c & 7);
+    }
+    static_cast<T*>(p.dst)[o] = from_f32<T>(v);
   }
 }
 

@@ -324,6 +324,8 @@ struct Model {
   double* abar = nullptr;
   int cus = 256;                 // compute units of the device (GEMM planning)
   void* zero = nullptr;          // 256 zero bytes: implicit-conv padding reads
+  float* split_ws = nullptr;     // split-K partial slabs (largest need of one step's GEMMs)
+  size_t split_floats = 0;
   // shapes per layer output (for the executor)
   std::vector<int> act_h, act_w, act_c;
 };
@@ -381,6 +383,7 @@ struct Packer {
     p.Dp = Dp;
     p.Cin = Cin;
     p.Cinp = Cinp;
+    p.frag = m->bf && gemm_frag_layout(rows, cols) && ld == cols;
     if (m->bf)
       pack<bf16>(p, s);
     else
@@ -629,6 +632,10 @@ void size_workspace(Model* m, Sizer& z) {
 
 // ============================================================================ create / destroy
 
+namespace {
+size_t step_split_need(Model* m);  // executor section
+}  // namespace
+
 
 Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats, bool on_device) {
   const std::vector<TensorSpec> table = weight_table(cfg);
@@ -732,6 +739,8 @@ Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats,
     DN_HIP(hipMemset(m->vt_ctx, 0, std::max<size_t>(z.vt_ctx * m->n_kv_slots, 1) * e));
     DN_HIP(hipMemset(m->vt_self, 0, std::max<size_t>(z.vt_self, 1) * e));
     m->cus = prop.multiProcessorCount;
+    m->split_floats = step_split_need(m.get());
+    if (m->split_floats) DN_HIP(hipMalloc(&m->split_ws, m->split_floats * 4));
     abar_table(m->abar, cfg.n_train_steps, cfg.beta_start, cfg.beta_end, cfg.beta_schedule, s);
     DN_HIP(hipStreamSynchronize(s));
   } catch (...) {
@@ -748,6 +757,7 @@ void model_destroy(Model* m) {
   if (m->packed) (void)hipFree(m->packed);
   if (m->params) (void)hipFree(m->params);
   if (m->arena) (void)hipFree(m->arena);
+  if (m->split_ws) (void)hipFree(m->split_ws);
   delete m;
 }
 
@@ -760,11 +770,17 @@ template <typename T> struct Exec {
   hipStream_t s;
   int n;
   bool dry = false;  // walk the step without launching anything
+  size_t split_need = 0;  // dry walk: largest split-K workspace (floats) of the step
 
   void run_gemm(GemmParams& p) {
-    if (dry) return;
-    const GemmPlan g = gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus);
+    const GemmPlan g = gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus, p.vt == nullptr);
+    if (dry) {
+      split_need = std::max(split_need, gemm_workspace_floats(g, p.M, p.N));
+      return;
+    }
     p.zero16 = m->zero;
+    p.part = m->split_ws;
+    p.part_floats = m->split_floats;
     gemm<T>(p, g, s);
   }
 
@@ -1041,6 +1057,22 @@ template <typename T> struct Exec {
     }
   }
 };
+
+// Largest split-K workspace of one denoise step (a walk that plans every GEMM).
+size_t step_split_need(Model* m) {
+  if (m->bf) {
+    Exec<bf16> ex{m, nullptr, m->n};
+    ex.dry = true;
+    ex.prepare(nullptr, 1);
+    ex.unet(0);
+    return ex.split_need;
+  }
+  Exec<float> ex{m, nullptr, m->n};
+  ex.dry = true;
+  ex.prepare(nullptr, 1);
+  ex.unet(0);
+  return ex.split_need;
+}
 
 // Timesteps reach the device as kernel arguments (chunks of kTsChunk).
 void time_features(Model* m, const int32_t* ts, int n, hipStream_t s) {

@@ -22,8 +22,9 @@ ABI_VERSION = 1
 MAX_LEVELS = 4
 
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_unet_eps", "ac_lookup",
-            "ac_fetch_latent", "dn_op_linear", "dn_op_conv3x3", "dn_op_attention", "dn_op_groupnorm",
-            "dn_op_layernorm", "dn_op_linear_vt", "dn_destroy", "dn_last_error")
+            "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
+            "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_linear_vt", "dn_destroy",
+            "dn_last_error")
 
 
 class DnError(RuntimeError):
@@ -67,6 +68,8 @@ def _load():
         "dn_unet_eps": [P, P, I32, P, F32, P, P, P],
         "ac_lookup": [P, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
         "ac_fetch_latent": [P, I64, I64, I64, P, P],
+        "dn_packed_weight_elems": [I32, I32, I32, C.POINTER(I64)],
+        "dn_pack_weight": [I32, P, I32, I32, P, P],
         "dn_op_linear": [I32, P, P, P, P, I32, P, I32, I64, I32, I32, I32, P],
         "dn_op_conv3x3": [I32, P, I32, I32, I32, I32, I32, I32, P, P, P, P, P, I32, I32, P],
         "dn_op_attention": [I32, P, I32, P, I32, P, I32, P, I32, I32, I32, I32, I32, I32, F32, P],
@@ -205,6 +208,20 @@ def ac_fetch_latent(cache_latents, idx, latent, stream=None):
     n = cache_latents.shape[0]
     numel = cache_latents[0].numel()
     _check(lib.ac_fetch_latent(_ptr(cache_latents), n, numel, idx, _ptr(latent), _stream(stream)))
+
+
+def packed_weight_elems(dtype, N, K):
+    n = C.c_int64()
+    _check(lib.dn_packed_weight_elems(dtype, N, K, C.byref(n)))
+    return n.value
+
+
+def pack_weight(dtype, w, N, K, stream=None):
+    """Row-major device weight [N][K] (dtype elements) -> a new tensor in the GEMM's packed layout."""
+    import torch
+    out = torch.empty(packed_weight_elems(dtype, N, K), device=w.device, dtype=w.dtype)
+    _check(lib.dn_pack_weight(dtype, _ptr(w), N, K, _ptr(out), _stream(stream)))
+    return out
 
 
 def op_linear(dtype, x, w, bias, y, M, N, K, resid=None, resid_f32=False, y_f32=False, geglu=False, stream=None):

@@ -34,10 +34,13 @@ def _rng(seed):
 
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280),
-                                   (2048, 2048, 128), (8192, 512, 256)])
+                                   (2048, 2048, 128), (8192, 512, 256), (300, 1280, 2560), (77, 96, 1920),
+                                   (1000, 640, 5120), (129, 256, 704)])
 def test_linear(dtype, M, N, K):
-    """Shapes cover every tile plan: 64 x 64 (few tiles), 128 x 128 (>= one tile per CU)
-    and, in bf16, the direct-to-LDS 256 x 256 kernel (M >= 8192 with a tile per CU)."""
+    """Shapes cover every tile plan: in fp32 the register-staged 64 x 64 / 128 x 128
+    tiles; in bf16 the row-major kernels for N % 32 != 0 (N = 200) and the fragment-B
+    kernel with 128 x 128 and 128 x 256 tiles, with and without split-K (few tiles and
+    long K: 300 x 1280 x 2560, 1000 x 640 x 5120), ragged M and N tails."""
     announce(f"linear dtype={dtype} M={M} N={N} K={K}")
     r = _rng(M + N + K)
     x, xh = to_dev(r.standard_normal((M, K)), dtype)
@@ -45,9 +48,10 @@ def test_linear(dtype, M, N, K):
     b = r.standard_normal(N).astype(np.float32)
     res = r.standard_normal((M, N)).astype(np.float32)
     y = torch.empty((M, N), device=DEV, dtype=tdtype(dtype))
-    dn.op_linear(dtype, x, w, f32_dev(b), y, M, N, K)
+    wp = dn.pack_weight(dtype, w, N, K)
+    dn.op_linear(dtype, x, wp, f32_dev(b), y, M, N, K)
     yr = torch.empty((M, N), device=DEV, dtype=torch.float32)
-    dn.op_linear(dtype, x, w, f32_dev(b), yr, M, N, K, resid=f32_dev(res), resid_f32=True, y_f32=True)
+    dn.op_linear(dtype, x, wp, f32_dev(b), yr, M, N, K, resid=f32_dev(res), resid_f32=True, y_f32=True)
     torch.cuda.synchronize()
     ref = L.linear(xh, wh, b.astype(np.float64))
     assert rel_l2(host(y), ref) < TOL[dtype]
@@ -71,7 +75,7 @@ def test_linear_geglu(dtype, M, N, K):
     x, xh = to_dev(r.standard_normal((M, K)), dtype)
     w1 = (r.standard_normal((2 * N, K)) / math.sqrt(K)).astype(np.float32)
     b1 = r.standard_normal(2 * N).astype(np.float32)
-    wp, _ = to_dev(_interleave(w1, N), dtype)
+    wp = dn.pack_weight(dtype, to_dev(_interleave(w1, N), dtype)[0], 2 * N, K)
     w1h = host(to_dev(w1, dtype)[0])
     bp = _interleave(b1[:, None], N)[:, 0].copy()
     y = torch.empty((M, N), device=DEV, dtype=tdtype(dtype))
@@ -102,7 +106,8 @@ def test_conv3x3(dtype, n, H, W, Cin, Cout, up, stride):
     res = r.standard_normal((n, ho, wo, Cout)).astype(np.float32)
     resd, resh = to_dev(res, dtype)
     y = torch.empty((n, ho, wo, Cout), device=DEV, dtype=tdtype(dtype))
-    dn.op_conv3x3(dtype, x, n, H, W, Cin, wd, f32_dev(b), y, Cout, up=up, stride=stride, temb=f32_dev(temb),
+    wp = dn.pack_weight(dtype, wd, Cout, 9 * Cin)
+    dn.op_conv3x3(dtype, x, n, H, W, Cin, wp, f32_dev(b), y, Cout, up=up, stride=stride, temb=f32_dev(temb),
                   resid=resd)
     torch.cuda.synchronize()
     full = ref.transpose(0, 2, 3, 1) + temb[:, None, None, :] + resh
@@ -175,7 +180,7 @@ def test_linear_vt(dtype, M, seq, heads, dp, K):
     ld = (seq + 63) // 64 * 64
     y = torch.empty((M, 2 * P), device=DEV, dtype=tdtype(dtype))
     vt = torch.zeros((M // seq, heads, dp, ld), device=DEV, dtype=tdtype(dtype))
-    dn.op_linear_vt(dtype, x, w, f32_dev(b), y, M, N, K, 2 * P, vt, heads, dp, seq, ld)
+    dn.op_linear_vt(dtype, x, dn.pack_weight(dtype, w, N, K), f32_dev(b), y, M, N, K, 2 * P, vt, heads, dp, seq, ld)
     torch.cuda.synchronize()
     ref = L.linear(xh, wh, b.astype(np.float64))
     assert rel_l2(host(y), ref[:, :2 * P]) < TOL[dtype]
@@ -232,7 +237,7 @@ def test_sdxl_ff_in_geglu_sampled():
     w = (torch.randn((2 * N, K), device=DEV, generator=g) / math.sqrt(K)).to(torch.bfloat16)
     b = torch.randn(2 * N, device=DEV, generator=g)
     y = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
-    dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True)
+    dn.op_linear(dn.DN_BF16, x, dn.pack_weight(dn.DN_BF16, w, 2 * N, K), b, y, M, N, K, geglu=True)
     torch.cuda.synchronize()
     r = _rng(5)
     ms, ns = _sample_idx(r, (M, N), 512)
@@ -255,7 +260,7 @@ def test_sdxl_conv_top_level_sampled():
     w = (torch.randn((C, 3, 3, C), device=DEV, generator=g) / math.sqrt(9 * C)).to(torch.bfloat16)
     b = torch.randn(C, device=DEV, generator=g)
     y = torch.empty((n, H, W, C), device=DEV, dtype=torch.bfloat16)
-    dn.op_conv3x3(dn.DN_BF16, x, n, H, W, C, w, b, y, C)
+    dn.op_conv3x3(dn.DN_BF16, x, n, H, W, C, dn.pack_weight(dn.DN_BF16, w, C, 9 * C), b, y, C)
     torch.cuda.synchronize()
     r = _rng(6)
     xh, wh, bh, yh = host(x), host(w), host(b), host(y)
@@ -311,8 +316,9 @@ def test_sdxl_linear_shapes_sampled_and_deterministic(M, N, K):
     res = torch.randn((M, N), device=DEV, generator=g)
     y1 = torch.empty((M, N), device=DEV)
     y2 = torch.empty((M, N), device=DEV)
-    dn.op_linear(dn.DN_BF16, x, w, b, y1, M, N, K, resid=res, resid_f32=True, y_f32=True)
-    dn.op_linear(dn.DN_BF16, x, w, b, y2, M, N, K, resid=res, resid_f32=True, y_f32=True)
+    wp = dn.pack_weight(dn.DN_BF16, w, N, K)
+    dn.op_linear(dn.DN_BF16, x, wp, b, y1, M, N, K, resid=res, resid_f32=True, y_f32=True)
+    dn.op_linear(dn.DN_BF16, x, wp, b, y2, M, N, K, resid=res, resid_f32=True, y_f32=True)
     torch.cuda.synchronize()
     assert torch.equal(y1, y2)
     r = _rng(M + K)
