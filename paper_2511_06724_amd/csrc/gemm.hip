@@ -269,14 +269,15 @@ template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPl
 // (four). The plan minimises a cost model fitted to measured SD-XL GEMM times on MI355X
 // (bf16, weights streamed from HBM): a run takes ceil(units / slots) rounds, a round
 // costs the MFMA work of the units resident on a CU at a per-CU rate R plus a fixed
-// prologue / epilogue cost O, and a K split adds the fp32 slabs written and read by the
-// reduction. GEGLU needs 64-column value/gate pairs per wave (the 128 x 256 tile).
-GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split) {
+// prologue cost O; the epilogue adds E per million outputs, and a K split adds the fp32
+// slabs written and read by the reduction (only the extra slab reads when the consumer
+// sums the slabs itself). GEGLU needs 64-column value/gate pairs per wave (128 x 256).
+GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce) {
   struct Var {
     int bm, bn, wg;
-    double rate, fixed;  // FLOP per us per CU, us per round
+    double rate, fixed, epi;  // FLOP per us per CU, us per round, us per 1e6 outputs
   };
-  static const Var vars[] = {{128, 256, 2, 2.4e6, 8.0}, {128, 128, 2, 2.0e6, 5.0}, {64, 128, 4, 2.0e6, 2.0}};
+  static const Var vars[] = {{128, 256, 2, 2.4e6, 1.0, 2.0}, {128, 128, 2, 1.6e6, 3.0, 0.0}, {64, 128, 4, 1.6e6, 1.0, 0.0}};
   GemmPlan best{128, 256, 0};
   best.stages = 3;
   best.frag = 1;
@@ -291,8 +292,8 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split) {
       const long long slots = (long long)cus * v.wg;
       const long long rounds = (units + slots - 1) / slots;
       const double per_cu = std::max(1.0, (double)std::min(units, slots) / cus);
-      double t = rounds * (per_cu * 2.0 * v.bm * v.bn * ((double)K / sp) / v.rate + v.fixed);
-      if (sp > 1) t += 0.2 * (sp + 1.0) * M * N * 4.0 / 1e6 + 2.0;
+      double t = rounds * (per_cu * 2.0 * v.bm * v.bn * ((double)K / sp) / v.rate + v.fixed) + v.epi * M * N / 1e6;
+      if (sp > 1) t += fused_reduce ? 0.1 * (sp - 1.0) * M * N * 4.0 / 1e6 : 0.1 * (sp + 1.0) * M * N * 4.0 / 1e6 + 2.0;
       if (t < best_t) {
         best_t = t;
         best.bm = v.bm;
@@ -304,8 +305,9 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split) {
   return best;
 }
 
-template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split) {
-  if (sizeof(T) == 2 && gemm_frag_layout(N, K)) return frag_plan(M, N, K, geglu, cus, allow_split);
+template <typename T>
+GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce) {
+  if (sizeof(T) == 2 && gemm_frag_layout(N, K)) return frag_plan(M, N, K, geglu, cus, allow_split, fused_reduce);
   const long long t128 = (long long)ceil_div(M, 128) * ceil_div(N, 128);
   if (sizeof(T) == 2 && N >= 128 && K % 64 == 0 && M >= 8192) {
     const long long t256 = (long long)ceil_div(M, 256) * ceil_div(N, 256);
@@ -347,8 +349,8 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
     dispatch<T, false>(p, g, s);
 }
 
-template GemmPlan gemm_plan<float>(int, int, int, int, int, bool);
-template GemmPlan gemm_plan<bf16>(int, int, int, int, int, bool);
+template GemmPlan gemm_plan<float>(int, int, int, int, int, bool, bool);
+template GemmPlan gemm_plan<bf16>(int, int, int, int, int, bool, bool);
 template void gemm<float>(const GemmParams&, const GemmPlan&, hipStream_t);
 template void gemm<bf16>(const GemmParams&, const GemmPlan&, hipStream_t);
 

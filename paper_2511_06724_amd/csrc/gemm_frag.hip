@@ -69,8 +69,10 @@ template <int BM, int FN, int S> constexpr size_t frag_lds_bytes() {
 // 2 implicit 3x3 convolution (one source). SPLIT: write fp32 partial tiles.
 // D: B register buffers (B is loaded D stages ahead). WPE: waves per SIMD the register
 // allocation must allow (2: two workgroups share a CU, so one's prologue, barriers and
-// epilogue overlap the other's MFMAs).
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT>
+// epilogue overlap the other's MFMAs). PRE: read a whole LDS stage of A fragments one
+// stage ahead into registers (small tiles, whose few MFMAs per k-step cannot cover an
+// LDS read latency), instead of one k-step ahead.
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_frag_kernel(
     GemmParams p, int mt, int nt, int nsplit) {
   constexpr int FM = BM / 32;
@@ -80,8 +82,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
   constexpr int PW = BM / 32;  // DMA instructions (8 rows of 128 B) per wave per stage
   constexpr int NM = FM * FN;
   static_assert(D == 1 || D == 2, "one or two B buffers");
-  // S <= 3: the hand-over wait below also covers the prologue stages only up to S = 3
-  static_assert(S >= 2 && S <= 3, "2 or 3 LDS stages");
+  static_assert(S >= 2 && S <= 6, "2 to 6 LDS stages");
   static_assert(BM % 32 == 0 && BM <= 256, "BM");
 
   extern __shared__ __align__(16) unsigned char smem[];
@@ -231,63 +232,125 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
   };
 
   BReg bq[D];
-  // One k-step: [the DMA of a later A stage first, when `dma`], the next k-step's A
-  // fragments from LDS, this k-step's MFMAs and the B loads of stage kt + D for this
-  // k-step, interleaved one MFMA / one LDS read / a share of the VM loads.
-  auto kstep = [&](auto dma, int dma_kt, int dma_slot, int rd_slot, int rd_s, bf16x8* a_use, bf16x8* a_next,
-                   bf16x8* b_use, int bkt, int s, BReg& bb) {
-    if constexpr (decltype(dma)::value) issue_a(dma_kt, dma_slot);
-    read_a(rd_slot, rd_s, a_next);
-    mfmas(a_use, b_use);
-    load_b_step(bkt, s, bb);
-    if constexpr (decltype(dma)::value) __builtin_amdgcn_sched_group_barrier(0x020, PW, 0);
-    KSched<0, NM, FM, FN>::apply();
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  // prologue: A stages kt0 .. kt0 + S - 1 (every slot), B stages kt0 .. kt0 + D - 1; the
-  // wait covers A stages kt0 and kt0 + 1 (so the first hand-over needs no count of its own)
+  if constexpr (PRE) {
+    // Stage kt: hand-over first (this wave's DMA of stage kt + 1 landed: at most VM_PRE
+    // later VM loads pending; after the barrier every wave's has, and every wave is done
+    // with the slot of stage kt - 1, whose fragments it read a stage earlier and used),
+    // then the DMA of stage kt + S - 1 into that slot, the reads of all of stage kt + 1's
+    // fragments into the other register set, and stage kt's MFMAs from registers with the
+    // B loads of stage kt + D as B registers free up.
+    // VM loads after the DMA of stage kt + 1 (issued at the start of stage kt + 2 - S):
+    // 4 FN B loads of that stage, then S - 3 stages of PW DMA + 4 FN B loads. When that DMA
+    // came from the prologue (kt = kt0 + r, r <= S - 2; stage kt0 issues no DMA) the count
+    // is (S - 3) PW + 4 D FN + 4 r FN, enough once D + r >= S - 2; r = 0 is the prologue wait.
+    static_assert(S == 3 || (S == 4 && D >= 1), "stage read-ahead: 3 or 4 LDS stages");
+    constexpr int VM_PRE = 4 * FN + (S - 3) * (PW + 4 * FN);
+    static_assert(VM_PRE < 64 && (S - 2) * PW + D * 4 * FN < 64, "vmcnt range");
+    typedef bf16x8 AStage[4][FM];
+    AStage sa[2];
+    auto read_stage = [&](int slot, AStage& dst) {
 #pragma unroll
-  for (int s = 0; s < S; ++s) issue_a(kt0 + s, s);
+      for (int s = 0; s < 4; ++s) read_a(slot, s, dst[s]);
+    };
 #pragma unroll
-  for (int d = 0; d < D; ++d)
+    for (int s = 0; s < S; ++s) issue_a(kt0 + s, s);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) load_b_step(kt0 + d, s, bq[d]);
-  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((S - 2) * PW + D * 4 * FN));
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_sched_barrier(0);
-  read_a(0, 0, fa[0]);
-
-  // Stage kt (slot (kt - kt0) % S, B buffer bb): k-steps 0..2; the hand-over: this wave's
-  // DMA of stage kt + 1 has landed once at most VM_END later VM loads are pending, and
-  // after the barrier every wave's has, and every wave is done reading slot kt; then
-  // k-step 3 issues stage kt + S into that slot and reads stage kt + 1's first fragments.
-  // VM loads issued after the DMA of stage kt + 1 (made in k-step 3 of stage kt + 1 - S):
-  // B(3) of that stage, S - 2 whole stages (4 FN B loads + PW DMA each), B(0..2) of stage kt.
-  // Stage kt0 + 1 was waited for in the prologue; the DMA of stage kt0 + 2 (S = 3, in the
-  // prologue) is followed by D * 4 FN + 4 FN + PW + 3 FN >= VM_END loads.
-  constexpr int VM_END = 4 * FN + (S - 2) * (4 * FN + PW);
-  static_assert(VM_END < 64 && (S - 2) * PW + D * 4 * FN < 64, "vmcnt range");
-  auto stage = [&](int kt, BReg& bb) {
-    const int rel = kt - kt0;
-    const int slot = rel % S;
-    const int nslot = (rel + 1) % S;
-    kstep(std::false_type{}, 0, 0, slot, 1, fa[0], fa[1], bb[0], kt + D, 0, bb);
-    kstep(std::false_type{}, 0, 0, slot, 2, fa[1], fa[0], bb[1], kt + D, 1, bb);
-    kstep(std::false_type{}, 0, 0, slot, 3, fa[0], fa[1], bb[2], kt + D, 2, bb);
-    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(VM_END));
+    for (int d = 0; d < D; ++d)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) load_b_step(kt0 + d, s, bq[d]);
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((S - 2) * PW + D * 4 * FN));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    kstep(std::true_type{}, kt + S, slot, nslot, 0, fa[1], fa[0], bb[3], kt + D, 3, bb);
-  };
-
-  if constexpr (D == 2) {
-    for (int kt = kt0; kt < kt1; kt += 2) {
-      stage(kt, bq[0]);
-      if (kt + 1 < kt1) stage(kt + 1, bq[D - 1]);
+    read_stage(0, sa[0]);
+    auto pstage = [&](int kt, AStage& cur, AStage& nxt, BReg& bb) {
+      const int r = kt - kt0;
+      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(VM_PRE));
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      if (r >= 1) issue_a(kt + S - 1, (r - 1) % S);
+      read_stage((r + 1) % S, nxt);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        mfmas(cur[s], bb[s]);
+        load_b_step(kt + D, s, bb);
+      }
+      if (r >= 1) __builtin_amdgcn_sched_group_barrier(0x020, PW, 0);
+      KSched<0, 4 * NM, 4 * FM, 4 * FN>::apply();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    if constexpr (D == 2) {
+      for (int kt = kt0; kt < kt1; kt += 2) {
+        pstage(kt, sa[0], sa[1], bq[0]);
+        if (kt + 1 < kt1) pstage(kt + 1, sa[1], sa[0], bq[D - 1]);
+      }
+    } else {
+      for (int kt = kt0; kt < kt1; kt += 2) {
+        pstage(kt, sa[0], sa[1], bq[0]);
+        if (kt + 1 < kt1) pstage(kt + 1, sa[1], sa[0], bq[0]);
+      }
     }
   } else {
-    for (int kt = kt0; kt < kt1; ++kt) stage(kt, bq[0]);
+    BReg bq[D];
+    // One k-step: [the DMA of a later A stage first, when `dma`], the next k-step's A
+    // fragments from LDS, this k-step's MFMAs and the B loads of stage kt + D for this
+    // k-step, interleaved one MFMA / one LDS read / a share of the VM loads.
+    auto kstep = [&](auto dma, int dma_kt, int dma_slot, int rd_slot, int rd_s, bf16x8* a_use, bf16x8* a_next,
+                     bf16x8* b_use, int bkt, int s, BReg& bb) {
+      if constexpr (decltype(dma)::value) issue_a(dma_kt, dma_slot);
+      read_a(rd_slot, rd_s, a_next);
+      mfmas(a_use, b_use);
+      load_b_step(bkt, s, bb);
+      if constexpr (decltype(dma)::value) __builtin_amdgcn_sched_group_barrier(0x020, PW, 0);
+      KSched<0, NM, FM, FN>::apply();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // prologue: A stages kt0 .. kt0 + S - 1 (every slot), B stages kt0 .. kt0 + D - 1; the
+    // wait covers A stages kt0 .. kt0 + Q (see the hand-over below)
+    constexpr int Q = (S - 1 - D) > 1 ? (S - 1 - D) : 1;
+  #pragma unroll
+    for (int s = 0; s < S; ++s) issue_a(kt0 + s, s);
+  #pragma unroll
+    for (int d = 0; d < D; ++d)
+  #pragma unroll
+      for (int s = 0; s < 4; ++s) load_b_step(kt0 + d, s, bq[d]);
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((S - 1 - Q) * PW + D * 4 * FN));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    read_a(0, 0, fa[0]);
+
+    // Stage kt (slot (kt - kt0) % S, B buffer bb): k-steps 0..2; the hand-over: this wave's
+    // DMA of stage kt + 1 has landed once at most VM_END later VM loads are pending, and
+    // after the barrier every wave's has, and every wave is done reading slot kt; then
+    // k-step 3 issues stage kt + S into that slot and reads stage kt + 1's first fragments.
+    // VM loads issued after the DMA of stage kt + 1 (made in k-step 3 of stage kt + 1 - S):
+    // B(3) of that stage, S - 2 whole stages (4 FN B loads + PW DMA each), B(0..2) of stage kt.
+    // When stage kt + 1 (kt = kt0 + r) came from the prologue, the loads after its DMA are
+    // (S - 2 - r) PW + 4 D FN + r (4 FN + PW) + 3 FN, at least VM_END once D + r >= S - 1;
+    // the prologue itself waited for stages up to kt0 + Q, Q = max(1, S - 1 - D).
+    constexpr int VM_END = 4 * FN + (S - 2) * (4 * FN + PW);
+    static_assert(VM_END < 64 && (S - 1 - Q) * PW + D * 4 * FN < 64, "vmcnt range");
+    auto stage = [&](int kt, BReg& bb) {
+      const int rel = kt - kt0;
+      const int slot = rel % S;
+      const int nslot = (rel + 1) % S;
+      kstep(std::false_type{}, 0, 0, slot, 1, fa[0], fa[1], bb[0], kt + D, 0, bb);
+      kstep(std::false_type{}, 0, 0, slot, 2, fa[1], fa[0], bb[1], kt + D, 1, bb);
+      kstep(std::false_type{}, 0, 0, slot, 3, fa[0], fa[1], bb[2], kt + D, 2, bb);
+      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(VM_END));
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      kstep(std::true_type{}, kt + S, slot, nslot, 0, fa[1], fa[0], bb[3], kt + D, 3, bb);
+    };
+
+    if constexpr (D == 2) {
+      for (int kt = kt0; kt < kt1; kt += 2) {
+        stage(kt, bq[0]);
+        if (kt + 1 < kt1) stage(kt + 1, bq[D - 1]);
+      }
+    } else {
+      for (int kt = kt0; kt < kt1; ++kt) stage(kt, bq[0]);
+    }
   }
   // The loads past the range (zero block, clamped B) must land before LDS is reused.
   __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
@@ -398,31 +461,33 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, int ns
   epilogue_group<bf16>(p, m, n, v);
 }
 
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT>
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE>
 void launch_frag(const GemmParams& p, int nsplit, hipStream_t s) {
   constexpr size_t lds = frag_lds_bytes<BM, FN, S>();
   static bool attr_set = false;
   if (!attr_set) {
-    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT>),
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
     attr_set = true;
   }
   const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, 128 * FN);
-  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT>), dim3(mt * nt * nsplit), dim3(kThreads), lds,
+  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE>), dim3(mt * nt * nsplit), dim3(kThreads), lds,
                      s, p, mt, nt, nsplit);
   DN_HIP(hipGetLastError());
 }
 
-template <int BM, int FN, int S, int D, int WPE, int MODE>
+template <int BM, int FN, int S, int D, int WPE, int MODE, int PRE = 0>
 void run_frag(const GemmParams& p, int nsplit, hipStream_t s) {
-  if (nsplit > 1) {
-    launch_frag<BM, FN, S, D, WPE, MODE, true>(p, nsplit, s);
+  if (p.raw_partial) {
+    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE>(p, nsplit, s);
+  } else if (nsplit > 1) {
+    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE>(p, nsplit, s);
     const long long nq = (long long)p.M * (p.n_store / 4);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, p,
                        nsplit);
     DN_HIP(hipGetLastError());
   } else {
-    launch_frag<BM, FN, S, D, WPE, MODE, false>(p, 1, s);
+    launch_frag<BM, FN, S, D, WPE, MODE, false, PRE>(p, 1, s);
   }
 }
 
@@ -434,6 +499,11 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   if (g.bm == 128 && g.bn == 256 && g.stages == 2) return run_frag<128, 2, 3, 2, 1, MODE>(p, g.split, s);
   if (g.bm == 128 && g.bn == 128 && g.stages == 3) return run_frag<128, 1, 3, 2, 2, MODE>(p, g.split, s);
   if (g.bm == 64 && g.bn == 128 && g.stages == 3) return run_frag<64, 1, 3, 2, 4, MODE>(p, g.split, s);
+  if (g.bm == 64 && g.bn == 128 && g.stages == 13) return run_frag<64, 1, 3, 2, 3, MODE, 1>(p, g.split, s);
+  if (g.bm == 64 && g.bn == 128 && g.stages == 14) return run_frag<64, 1, 4, 2, 3, MODE, 1>(p, g.split, s);
+  if (g.bm == 128 && g.bn == 128 && g.stages == 13) return run_frag<128, 1, 3, 2, 2, MODE, 1>(p, g.split, s);
+  if (g.bm == 64 && g.bn == 256 && g.stages == 13) return run_frag<64, 2, 3, 2, 2, MODE, 1>(p, g.split, s);
+  if (g.bm == 32 && g.bn == 128 && g.stages == 13) return run_frag<32, 1, 3, 2, 4, MODE, 1>(p, g.split, s);
   throw Error(-1, "gemm: no fragment-B kernel for this tile plan");
 }
 
@@ -479,7 +549,7 @@ void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
   DN_CHECK(p.taps == 1 || p.c1 == 0, "gemm: the fragment-B conv takes one input source");
   DN_CHECK(g.split >= 1 && g.split <= kMaxSplit && p.K / kBK >= g.split, "gemm: bad split");
   DN_CHECK(!p.geglu || (g.bn / 4) % 64 == 0, "gemm: GEGLU needs 64-column value/gate pairs per wave");
-  if (g.split > 1) {
+  if (g.split > 1 || p.raw_partial) {
     DN_CHECK(!p.geglu && !p.vt, "gemm: split-K takes neither GEGLU nor the V^T output");
     DN_CHECK(p.n_store % 4 == 0 && p.n_store == p.N, "gemm: split-K needs n_store == N, a multiple of 4");
     DN_CHECK(p.part && p.part_floats >= (size_t)g.split * p.M * p.n_store, "gemm: split-K workspace too small");

@@ -46,6 +46,9 @@ struct GemmParams {
   // Split-K workspace (fragment-B kernel): fp32 partial slabs [split][M][n_store].
   float* part = nullptr;
   size_t part_floats = 0;
+  // Raw partial output: write the slabs (even unsplit) and skip the reduction and the
+  // epilogue; a later kernel (layernorm_reduce) completes them.
+  int raw_partial = 0;
 };
 
 // Block tile (bm x bn) of one GEMM launch and the kernel that runs it.
@@ -58,8 +61,11 @@ struct GemmPlan {
   int split = 1;         // fragment-B kernel: K split in this many ranges (fp32 partials + reduce)
 };
 constexpr int kMaxSplit = 8;
-// allow_split = false for epilogues split-K does not support (the per-head V^T output).
-template <typename T> GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split = true);
+// allow_split = false for epilogues split-K does not support (the per-head V^T output);
+// fused_reduce: the partial slabs are summed by the consumer (layernorm_reduce), so a
+// split costs only the extra slab reads.
+template <typename T>
+GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split = true, bool fused_reduce = false);
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 void gemm_bf16_dma(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s);
@@ -70,8 +76,8 @@ bool gemm_frag_layout(int N, int K);
 size_t gemm_frag_elems(int N, int K);  // N rounded up to 32, times K
 void to_frag(const bf16* src, int N, int K, int ld_src, bf16* dst, hipStream_t s);
 // fp32 workspace floats the plan needs (split-K partial slabs), 0 when none.
-inline size_t gemm_workspace_floats(const GemmPlan& g, int M, int N) {
-  return g.frag && g.split > 1 ? (size_t)g.split * M * N : 0;
+inline size_t gemm_workspace_floats(const GemmPlan& g, int M, int N, bool raw_partial = false) {
+  return g.frag && (g.split > 1 || raw_partial) ? (size_t)g.split * M * N : 0;
 }
 template <typename T> constexpr int gemm_bk() { return sizeof(T) == 2 ? 64 : 32; }
 
@@ -114,6 +120,11 @@ template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s);
 template <typename T>
 void layernorm(const float* x, T* y, long long M, int C, const float* gamma, const float* beta, float eps,
                hipStream_t s);
+// LayerNorm that first completes a residual update: x = (resid ? x : 0) + bias +
+// sum_s part[s] (nsplit fp32 slabs [M][C], summed in order), written back to x.
+template <typename T>
+void layernorm_reduce(float* x, T* y, long long M, int C, const float* gamma, const float* beta, float eps,
+                      const float* part, int nsplit, const float* bias, bool resid, hipStream_t s);
 
 // ---------------------------------------------------------------- misc
 void abar_table(double* abar, int T, double beta_start, double beta_end, int schedule, hipStream_t s);

@@ -912,16 +912,65 @@ template <typename T> struct Exec {
     if (!dry) attention<T>(a, x.Dp, s);
   }
 
+  // A residual-stream update R = (resid ? R : 0) + x W^T + b whose result is layer-normalised
+  // next (a = LN(R)). When the plan splits K, the GEMM writes fp32 partial slabs only and
+  // one LayerNorm pass sums them with the bias and R, writes R and normalises (no separate
+  // reduction kernel); otherwise the GEMM epilogue updates R and a plain LayerNorm follows.
+  struct Pending {
+    const LinW* w = nullptr;
+    int nsplit = 0;   // 0: R already final
+    bool resid = true;
+  };
+  Pending residual_gemm(const LinW& w, const void* x, int ldx, long long M, bool resid) {
+    const GemmPlan g = gemm_plan<T>(static_cast<int>(M), w.n, w.k, 0, m->cus, true, true);
+    if (!g.frag || g.split == 1) {
+      linear(w, x, ldx, M, m->R, w.n, true, resid ? m->R : nullptr, w.n, true);
+      return Pending{};
+    }
+    GemmParams p;
+    p.a0 = x;
+    p.c0 = w.k;
+    p.lda0 = ldx;
+    p.taps = 1;
+    p.b = w.w;
+    p.ldb = w.k;
+    p.M = static_cast<int>(M);
+    p.N = w.n;
+    p.K = w.k;
+    p.out = m->R;
+    p.ldo = w.n;
+    p.out_f32 = 1;
+    p.n_store = w.n;
+    p.raw_partial = 1;
+    if (dry) {
+      split_need = std::max(split_need, gemm_workspace_floats(g, p.M, p.N, true));
+    } else {
+      p.zero16 = m->zero;
+      p.part = m->split_ws;
+      p.part_floats = m->split_floats;
+      gemm<T>(p, g, s);
+    }
+    return Pending{&w, g.split, resid};
+  }
+  void ln_after(const Pending& pd, long long M, int C, const Norm& nm) {
+    if (dry) return;
+    if (pd.nsplit)
+      layernorm_reduce<T>(m->R, P_<T>(m->a), M, C, nm.g, nm.b, m->cfg.ln_eps, m->split_ws, pd.nsplit, pd.w->b,
+                          pd.resid, s);
+    else
+      layernorm<T>(m->R, P_<T>(m->a), M, C, nm.g, nm.b, m->cfg.ln_eps, s);
+  }
+
   void transformer(const TxL& x, const void* in, int H, int W, void* out) {
     const int HW = H * W, C = x.c, P = x.heads * x.Dp;
     const long long M = (long long)n * HW;
     const size_t e = sizeof(T);
     groupnorm_(in, C, nullptr, 0, HW, x.gn, m->cfg.tx_gn_eps, false, m->gn_out);
-    linear(x.proj_in, m->gn_out, C, M, m->R, C, true);
+    Pending pd = residual_gemm(x.proj_in, m->gn_out, C, M, false);
     for (size_t bi = 0; bi < x.blocks.size(); ++bi) {
       const TxBlock& b = x.blocks[bi];
       const bool last = bi + 1 == x.blocks.size();
-      if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln1.g, b.ln1.b, m->cfg.ln_eps, s);
+      ln_after(pd, M, C, b.ln1);
       // Q and K land in qkv [M][2P]; V goes to vt_self transposed per head.
       const int ld_self = (HW + 63) / 64 * 64;
       VtOut vs;
@@ -935,18 +984,18 @@ template <typename T> struct Exec {
       const char* qkv = static_cast<const char*>(m->qkv);
       attention_(qkv, 2 * P, (long long)HW * 2 * P, qkv + (size_t)P * e, 2 * P, (long long)HW * 2 * P, m->vt_self,
                  ld_self, HW, HW, x);
-      linear(b.o1, m->o, P, M, m->R, C, true, m->R, C, true);
-      if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln2.g, b.ln2.b, m->cfg.ln_eps, s);
+      pd = residual_gemm(b.o1, m->o, P, M, true);
+      ln_after(pd, M, C, b.ln2);
       linear(b.q2, m->a, C, M, m->q2, P, false);
       const char* kv = static_cast<const char*>(m->kv) + (size_t)b.kv_slot * m->kv_slot_elems * e;
       const char* vtc = static_cast<const char*>(m->vt_ctx) + (size_t)b.kv_slot * m->vt_ctx_slot_elems * e;
       attention_(m->q2, P, (long long)HW * P, kv, P, (long long)m->cfg.ctx_len * P, vtc,
                  (m->cfg.ctx_len + 63) / 64 * 64, HW, m->cfg.ctx_len, x);
-      linear(b.o2, m->o, P, M, m->R, C, true, m->R, C, true);
-      if (!dry) layernorm<T>(m->R, P_<T>(m->a), M, C, b.ln3.g, b.ln3.b, m->cfg.ln_eps, s);
+      pd = residual_gemm(b.o2, m->o, P, M, true);
+      ln_after(pd, M, C, b.ln3);
       linear(b.ff1, m->a, C, M, m->ff, m->cfg.ff_mult * C, false, nullptr, 0, false, true);
       if (!last)
-        linear(b.ff2, m->ff, m->cfg.ff_mult * C, M, m->R, C, true, m->R, C, true);
+        pd = residual_gemm(b.ff2, m->ff, m->cfg.ff_mult * C, M, true);
       else
         linear(b.ff2, m->ff, m->cfg.ff_mult * C, M, m->rt, C, false, m->R, C, true);
     }

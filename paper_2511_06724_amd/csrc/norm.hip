@@ -206,21 +206,47 @@ template <> struct Store4<float> {
   }
 };
 
+// One wave per row. With nsplit > 0 the row is first rebuilt from the residual stream:
+// x[row] = (resid ? x[row] : 0) + bias + sum_s part[s][row] in that order (the reduction of
+// a split-K GEMM that wrote fp32 partial slabs), and written back; then
+// y = (x - mean) * rstd * gamma + beta with two-pass mean / variance.
 template <typename T>
-__global__ __launch_bounds__(256) void ln_kernel(const float* x, T* y, long long M, int C, const float* gamma,
-                                                 const float* beta, float eps) {
+__global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, int C, const float* gamma,
+                                                 const float* beta, float eps, const float* part, int nsplit,
+                                                 long long slab, const float* bias, int resid) {
   const int lane = threadIdx.x & 63;
   const long long row = blockIdx.x * 4ll + (threadIdx.x >> 6);
   if (row >= M) return;
   const int nv = C / 4;
-  const float4* xr = reinterpret_cast<const float4*>(x + row * C);
+  float4* xr = reinterpret_cast<float4*>(x + row * C);
   float4 v[kLnMaxVec];
   float s = 0.f;
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
     const int i = lane + 64 * j;
     if (i < nv) {
-      v[j] = xr[i];
+      if (nsplit > 0) {
+        float4 a = resid ? xr[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+        if (bias) {
+          const float4 b = reinterpret_cast<const float4*>(bias)[i];
+          a.x += b.x;
+          a.y += b.y;
+          a.z += b.z;
+          a.w += b.w;
+        }
+        const float4* pr = reinterpret_cast<const float4*>(part + row * C);
+        for (int k = 0; k < nsplit; ++k) {
+          const float4 t = pr[k * (slab / 4) + i];
+          a.x += t.x;
+          a.y += t.y;
+          a.z += t.z;
+          a.w += t.w;
+        }
+        xr[i] = a;
+        v[j] = a;
+      } else {
+        v[j] = xr[i];
+      }
       s += (v[j].x + v[j].y) + (v[j].z + v[j].w);
     }
   }
@@ -277,12 +303,20 @@ template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s) {
 template <typename T>
 void layernorm(const float* x, T* y, long long M, int C, const float* gamma, const float* beta, float eps,
                hipStream_t s) {
+  layernorm_reduce<T>(const_cast<float*>(x), y, M, C, gamma, beta, eps, nullptr, 0, nullptr, true, s);
+}
+
+template <typename T>
+void layernorm_reduce(float* x, T* y, long long M, int C, const float* gamma, const float* beta, float eps,
+                      const float* part, int nsplit, const float* bias, bool resid, hipStream_t s) {
   DN_CHECK(M >= 1 && C >= 4 && C % 4 == 0 && C <= 4 * 64 * kLnMaxVec, "layernorm: C must be a multiple of 4, <= 2048");
   DN_CHECK(x && y && gamma && beta, "layernorm: null");
-  DN_CHECK(((uintptr_t)x | (uintptr_t)gamma | (uintptr_t)beta) % 16 == 0 && (uintptr_t)y % (4 * sizeof(T)) == 0,
-           "layernorm: x, gamma and beta must be 16-byte aligned, y aligned to 4 elements");
+  DN_CHECK(((uintptr_t)x | (uintptr_t)gamma | (uintptr_t)beta | (uintptr_t)part | (uintptr_t)bias) % 16 == 0 &&
+               (uintptr_t)y % (4 * sizeof(T)) == 0,
+           "layernorm: x, gamma, beta, partials and bias must be 16-byte aligned, y aligned to 4 elements");
+  DN_CHECK(nsplit == 0 || part, "layernorm: partial slabs missing");
   hipLaunchKernelGGL(ln_kernel<T>, dim3(static_cast<unsigned>((M + 3) / 4)), dim3(256), 0, s, x, y, M, C, gamma,
-                     beta, eps);
+                     beta, eps, part, nsplit, M * C, bias, resid ? 1 : 0);
   DN_HIP(hipGetLastError());
 }
 
@@ -290,5 +324,9 @@ template void groupnorm<float>(const GroupNormParams&, hipStream_t);
 template void groupnorm<bf16>(const GroupNormParams&, hipStream_t);
 template void layernorm<float>(const float*, float*, long long, int, const float*, const float*, float, hipStream_t);
 template void layernorm<bf16>(const float*, bf16*, long long, int, const float*, const float*, float, hipStream_t);
+template void layernorm_reduce<float>(float*, float*, long long, int, const float*, const float*, float, const float*,
+                                      int, const float*, bool, hipStream_t);
+template void layernorm_reduce<bf16>(float*, bf16*, long long, int, const float*, const float*, float, const float*,
+                                     int, const float*, bool, hipStream_t);
 
 }  // namespace dn
