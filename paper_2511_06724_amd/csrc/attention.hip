@@ -231,41 +231,43 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16, head dim 64: direct-to-LDS variant for long key ranges.
+// bf16, head dim 64: software-pipelined kernel for long key ranges.
 //
-// Same math as attn_kernel, organised like the direct-to-LDS GEMM:
-//  - a workgroup covers NQ x 32 queries of one (sample, head); workgroup ids are
-//    mapped so that consecutive ids of one XCD walk the query tiles of the same
-//    heads, which keeps those heads' K / V^T in that XCD's L2;
-//  - NQ query groups of 32 x NK key groups of waves: wave (wq, wk) takes queries
-//    [q0 + 32 wq, +32) and, of every NK consecutive key tiles (a tile group), tile
-//    wk; the NK partial softmax states (reference max, row sum, unnormalised O) of a
-//    query group are merged through LDS at the end (twice the waves of a one-pass
-//    kernel for the same queries);
-//  - key tiles of 64 (K rows of 128 bytes and the 64 V^T rows of 64 keys, 16 KB)
-//    go global -> LDS with global_load_lds_dwordx4 into a ring of kRing tile
-//    groups: a hand-over retires one group and refills its slots with the group
-//    kRing ahead; past the last group the last one is loaded again (the same count
-//    of loads per hand-over; nothing reads it);
-//  - 128-byte LDS rows without padding, chunk c of row r at c ^ f(r),
-//    f(r) = (r & 7) ^ ((r >> 3) & 1) (conflict-free 16-byte fragment reads);
-//  - every K fragment of a tile is read before the S MFMAs, every V^T fragment
-//    before the PV MFMAs; row max and sum use independent partial reductions.
-constexpr int kRing = 2;  // ring depth in tile groups
-
-template <int NQ, int NK>
-__global__ __launch_bounds__(64 * NQ * NK) void attn_dma_kernel(AttnParams p, int qtiles) {
-  constexpr int NW = NQ * NK;
+// Same math as attn_kernel. A workgroup covers NQ x 32 queries of one (sample,
+// head); workgroup ids are dealt so that each XCD (ids congruent mod 8) holds a
+// contiguous range of heads, whose K and V^T then stay in that XCD's L2. Key tiles of
+// 64 (K rows and the V^T rows of those keys, 16 KB) go global -> LDS with
+// global_load_lds_dwordx4 into a ring of R tiles. Per key tile g every wave
+//  - passes a hand-over (its loads of the tile it needs next landed, then a barrier:
+//    everyone's have, and everyone is done with tile g - 1's slot) and issues tile
+//    g + R - 1 into that slot;
+//  - with score read-ahead (PIPE): reads K of tile g + 1 and V^T of tile g from LDS,
+//    takes tile g's row maximum, then issues the S^T = K Q^T MFMAs of tile g + 1
+//    interleaved with the exponentials of tile g, and O^T += V^T P^T for tile g;
+//    without: scores and softmax of tile g in turn.
+// Within each 16-key group the K tile holds its keys in the order of bit 2 and bit 3
+// of the key index swapped: score register 8c + e of a 32-key block then belongs to
+// key 16c + 8h + e (h = lane half), so the V^T operand of a P fragment is 8
+// consecutive keys, one 16-byte LDS read. The row sum is taken on the bf16
+// probabilities that enter the P V product (dot products with (1, 1)); the partner
+// lane's statistics come over v_permlane32_swap. The score and output accumulators
+// stay in VGPRs (WPE waves per SIMD); only the last tile can hold key padding
+// (masked). Row maxima need no NaN quieting (this file is built without NaN
+// semantics: every input is finite and key padding is -inf, never NaN).
+template <int NQ, int R, int WPE, bool PIPE>
+__global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void attn_pipe_kernel(
+    AttnParams p, int qtiles) {
   constexpr int D = 64;
   constexpr int ROWB = 128;                  // bytes per LDS row (64 bf16)
   constexpr int TILE = 2 * kKT * ROWB;       // K tile then V^T tile (16 KB)
   constexpr int TI = 2 * kKT / 8;            // DMA instructions per tile (8 rows each)
-  constexpr int PW = NK * TI / NW;           // per wave per hand-over
-  static_assert((NK * TI) % NW == 0, "DMA instructions must divide over the waves");
+  constexpr int PW = TI / NQ;                // per wave per tile
+  constexpr int U = R % 2 == 0 ? R : 2 * R;  // unroll: ring slot and score buffer fixed
+  static_assert(TI % NQ == 0, "DMA instructions must divide over the waves");
+  static_assert(R >= (PIPE ? 3 : 2) && R <= 5, "ring of 3 (2 without score read-ahead) to 5 tiles");
 
   extern __shared__ __align__(16) unsigned char smem[];
 
-  // ---- (query tile, head, sample) of this workgroup, XCD-contiguous
   const int total = qtiles * p.heads * p.B;
   const int wg = blockIdx.x;
   const int xcd = wg % 8, idx = wg / 8;
@@ -277,9 +279,8 @@ __global__ __launch_bounds__(64 * NQ * NK) void attn_dma_kernel(AttnParams p, in
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wq = wave % NQ, wk = wave / NQ;
   const int half = lane >> 5;
-  const int q0 = qt * (32 * NQ) + wq * 32;
+  const int q0 = qt * (32 * NQ) + wave * 32;
 
   const bf16* qp = static_cast<const bf16*>(p.q) + b * p.q_bs + h * D;
   const bf16* kp = static_cast<const bf16*>(p.k) + b * p.k_bs + h * D;
@@ -293,37 +294,87 @@ __global__ __launch_bounds__(64 * NQ * NK) void attn_dma_kernel(AttnParams p, in
       qf[s] = *reinterpret_cast<const bf16x8*>(qp + (long long)qrow * p.ldq + s * 16 + half * 8);
   }
 
-  // ---- DMA: instruction j of this wave fills rows [8 r, 8 r + 8) of tile (i / TI) of the
-  // group, r = i % TI, i = wave * PW + j (rows 0..63: keys of K, 64..127: V^T head dims);
-  // the lane fetches logical chunk (lane & 7) ^ f(row). Groups past the last one load
-  // the last group again (same count of loads per hand-over; nothing reads them).
+  // DMA: instruction i = wave * PW + j of a tile fills rows [8 i, 8 i + 8) of its ring
+  // slot (rows 0..63: K, the key of row r being k0 + swap23(r); rows 64..127: V^T
+  // head dims); the lane fetches logical chunk (lane & 7) ^ f(row). A wave's rows are
+  // all K or all V^T (8 DMA rows per wave group), so its source is a wave-uniform
+  // base, advanced by one tile per issue, plus fixed 32-bit lane offsets; only the
+  // last tile (key rows clamped to Skv - 1) sets its offsets again. Issues past the
+  // last tile load the last one again (the same count of loads per hand-over; nothing
+  // reads them).
   const int lrow = lane >> 3;
   const int ntiles = (p.Skv + kKT - 1) / kKT;
-  const int ngroups = (ntiles + NK - 1) / NK;
-  auto issue = [&](int grp_in, int gslot) {
-    const int grp = min(grp_in, ngroups - 1);
+  auto swap23 = [](int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); };
+  const bool k_rows = wave * PW < kKT / 8;
+  const char* gbase = k_rows ? reinterpret_cast<const char*>(kp) : reinterpret_cast<const char*>(vtp);
+  const long long gstep = k_rows ? (long long)kKT * p.ldk * 2 : kKT * 2;
+  unsigned goff[PW];
+  auto set_offsets = [&](int t) {
+    const int k0 = t * kKT;
 #pragma unroll
     for (int j = 0; j < PW; ++j) {
       const int i = wave * PW + j;
-      const int tt = i / TI, r = i % TI;
-      const int t = min(grp * NK + tt, ntiles - 1);
-      const int k0 = t * kKT;
-      const int row = 8 * r + lrow;
-      const int lc = ((lane & 7) ^ lrow ^ (r & 1)) * 8;
-      const bf16* g;
-      if (r < kKT / 8) {
-        const int key = min(k0 + row, p.Skv - 1);
-        g = kp + (long long)key * p.ldk + lc;
-      } else {
-        g = vtp + (long long)(row - kKT) * p.vt_ld + k0 + lc;
-      }
-      __builtin_amdgcn_global_load_lds((gbl_void_t*)g,
-                                       (lds_void_t*)(smem + (gslot * NK + tt) * TILE + r * 1024), 16, 0, 0);
+      const int row = 8 * i + lrow;
+      const int lc = ((lane & 7) ^ lrow ^ (i & 1)) * 8;
+      if (k_rows)
+        goff[j] = 2u * (unsigned)(min(k0 + swap23(row), p.Skv - 1) - k0) * (unsigned)p.ldk + 2u * lc;
+      else
+        goff[j] = 2u * (unsigned)((row - kKT) * p.vt_ld + lc);
+    }
+  };
+  set_offsets(0);
+  int next_issue = 0;
+  auto issue = [&](int slot) {
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int i = wave * PW + j;
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(gbase + goff[j]), (lds_void_t*)(smem + slot * TILE + i * 1024), 16,
+                                       0, 0);
+    }
+    if (next_issue < ntiles - 1) {
+      ++next_issue;
+      gbase += gstep;
+      if (next_issue == ntiles - 1) set_offsets(next_issue);
     }
   };
 
   const int frow = lane & 31;
   const int fs = (lane & 7) ^ ((lane >> 3) & 1);
+  // lane byte offsets: K fragment of k-step s (key block kb adds 32 rows), V^T
+  // fragment of key chunk 4 kb + 2 c + h (head-dim block d adds 32 rows)
+  int koff[4], voff[2][2];
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2) koff[s2] = frow * ROWB + ((2 * s2 + half) ^ fs) * 16;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) voff[kb][c] = kKT * ROWB + frow * ROWB + ((4 * kb + 2 * c + half) ^ fs) * 16;
+
+  auto load_k = [&](const unsigned char* T, bf16x8 (&kf)[2][4]) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int s2 = 0; s2 < 4; ++s2) kf[kb][s2] = *reinterpret_cast<const bf16x8*>(T + kb * 32 * ROWB + koff[s2]);
+  };
+  auto load_v = [&](const unsigned char* T, bf16x8 (&vf)[2][2][2]) {
+#pragma unroll
+    for (int d = 0; d < 2; ++d)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) vf[d][kb][c] = *reinterpret_cast<const bf16x8*>(T + d * 32 * ROWB + voff[kb][c]);
+  };
+  // S^T = K Q^T for the 64 keys of a tile (two 32-key blocks)
+  auto mfma_scores = [&](const bf16x8 (&kf)[2][4], f32x16* sa) {
+    const f32x16 zero = {};
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sa[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb][0], qf[0], zero, 0, 0, 0);
+#pragma unroll
+    for (int s2 = 1; s2 < 4; ++s2)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        sa[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb][s2], qf[s2], sa[kb], 0, 0, 0);
+  };
 
   f32x16 o[2];
 #pragma unroll
@@ -331,154 +382,131 @@ __global__ __launch_bounds__(64 * NQ * NK) void attn_dma_kernel(AttnParams p, in
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[d][r] = 0.f;
   float m_ref = -INFINITY, l_run = 0.f;
+  f32x16 sacc[2][2];
 
-#pragma unroll
-  for (int g = 0; g < kRing; ++g) issue(g, g);
-  __builtin_amdgcn_s_waitcnt(attn_wait_vm_lgkm0((kRing - 1) * PW));
-  __builtin_amdgcn_s_barrier();
+  // value of x in lane l ^ 32 (lanes l and l ^ 32 hold one query's two key halves)
+  auto partner = [](float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                                    false, false);
+    return __builtin_bit_cast(float, (threadIdx.x & 32) ? r[0] : r[1]);
+  };
 
-  int gslot = 0;
-  for (int grp = 0; grp < ngroups; ++grp) {
-    const int t = grp * NK + wk;
-    if (t < ntiles) {
-      const int k0 = t * kKT;
-      const unsigned char* Ks = smem + (gslot * NK + wk) * TILE;
-      const unsigned char* Vs = Ks + kKT * ROWB;
-
-      // S^T = K Q^T for 64 keys (two 32-key blocks): every K fragment first
-      bf16x8 kf[2][4];
+  // softmax, first part: key padding of the last tile, the tile's row maximum, and a
+  // move of the reference maximum (rescaling O and l) when it grew by more than kLazy
+  auto softmax_max = [&](int k0, f32x16* sa) {
+    if (k0 + kKT > p.Skv) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
-          kf[kb][s] = *reinterpret_cast<const bf16x8*>(Ks + (kb * 32 + frow) * ROWB + ((2 * s + half) ^ fs) * 16);
-      f32x16 sacc[2];
+        for (int r = 0; r < 16; ++r)
+          if (k0 + kb * 32 + 16 * (r >> 3) + 8 * half + (r & 7) >= p.Skv) sa[kb][r] = -INFINITY;
+    }
+    float mc[4];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb][s], qf[s], sacc[kb], 0, 0, 0);
-
-      // V^T fragments: keys in the accumulator order of P (two 8-byte reads each)
-      bf16x8 vf[2][2][2];
+    for (int j = 0; j < 4; ++j) {
+      float m = fmaxf(fmaxf(sa[0][4 * j], sa[0][4 * j + 1]), sa[0][4 * j + 2]);
+      m = fmaxf(fmaxf(m, sa[0][4 * j + 3]), sa[1][4 * j]);
+      m = fmaxf(fmaxf(m, sa[1][4 * j + 1]), sa[1][4 * j + 2]);
+      mc[j] = fmaxf(m, sa[1][4 * j + 3]);
+    }
+    float mx = fmaxf(fmaxf(mc[0], mc[1]), fmaxf(mc[2], mc[3]));
+    mx = fmaxf(mx, partner(mx)) * p.scale_log2;
+    if (__any(mx > m_ref + kLazy)) {
+      const float m_new = fmaxf(m_ref, mx);
+      const float alpha = fast_exp2(m_ref - m_new);
+      l_run *= alpha;
 #pragma unroll
       for (int d = 0; d < 2; ++d)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+      m_ref = m_new;
+    }
+  };
+  // softmax, second part: P = 2^(s scale - m) in bf16, its row sum, O^T += V^T P^T
+  auto softmax_pv = [&](const f32x16* sa, const bf16x8 (&vf)[2][2][2]) {
+    bf16x8 pf[2][2];
+    float sp[2] = {0.f, 0.f};
+    const bf16x2 ones = {static_cast<bf16>(1.f), static_cast<bf16>(1.f)};
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int lo = 4 * kb + 2 * c;
-            const unsigned char* row = Vs + (d * 32 + frow) * ROWB + 8 * half;
-            const bf16x4 a = *reinterpret_cast<const bf16x4*>(row + ((lo ^ fs) * 16));
-            const bf16x4 bq = *reinterpret_cast<const bf16x4*>(row + (((lo + 1) ^ fs) * 16));
-            bf16x8 v;
-            v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
-            v[4] = bq[0]; v[5] = bq[1]; v[6] = bq[2]; v[7] = bq[3];
-            vf[d][kb][c] = v;
-          }
-
-      if (k0 + kKT > p.Skv) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      for (int c = 0; c < 2; ++c) {
+        bf16x8 pv;
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (k0 + kb * 32 + acc_row(r, lane) >= p.Skv) sacc[kb][r] = -INFINITY;
+        for (int e = 0; e < 8; ++e) pv[e] = static_cast<bf16>(fast_exp2(sa[kb][8 * c + e] * p.scale_log2 - m_ref));
+        pf[kb][c] = pv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bf16x2 pair = {pv[2 * e], pv[2 * e + 1]};
+          sp[e & 1] = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, sp[e & 1], false);
+        }
       }
-
-      // row max: four independent partial maxima, then the partner lane
-      float mp[4];
+    const float rs = sp[0] + sp[1];
+    l_run += rs + partner(rs);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        mp[i] = fmaxf(fmaxf(fmaxf(sacc[0][i], sacc[0][4 + i]), fmaxf(sacc[0][8 + i], sacc[0][12 + i])),
-                      fmaxf(fmaxf(sacc[1][i], sacc[1][4 + i]), fmaxf(sacc[1][8 + i], sacc[1][12 + i])));
-      float mx = fmaxf(fmaxf(mp[0], mp[1]), fmaxf(mp[2], mp[3]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
-      if (__any(mx > m_ref + kLazy)) {
-        const float m_new = fmaxf(m_ref, mx);
-        const float alpha = fast_exp2(m_ref - m_new);
-        l_run *= alpha;
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int d = 0; d < 2; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
-        m_ref = m_new;
-      }
-      bf16x8 pf[2][2];
-      float sp[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          bf16x8 pv;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float ex = fast_exp2(sacc[kb][8 * c + e] * p.scale_log2 - m_ref);
-            sp[e & 3] += ex;
-            pv[e] = static_cast<bf16>(ex);
-          }
-          pf[kb][c] = pv;
-        }
-      const float rs = (sp[0] + sp[1]) + (sp[2] + sp[3]);
-      l_run += rs + __shfl_xor(rs, 32, 64);
+          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[d][kb][c], pf[kb][c], o[d], 0, 0, 0);
+  };
 
-      // O^T += V^T P^T
+  // prologue: tiles 0 .. R - 2 in flight (with score read-ahead: tile 0 landed
+  // everywhere, its scores taken)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-          for (int d = 0; d < 2; ++d)
-            o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[d][kb][c], pf[kb][c], o[d], 0, 0, 0);
-    }
-
-    // hand-over: group grp + 1 (the last one issued) must have landed; after the barrier
-    // every wave is done with group grp's slots, which take group grp + kRing
-    __builtin_amdgcn_s_waitcnt(attn_wait_vm_lgkm0((kRing - 2) * PW));
+  for (int t = 0; t < R - 1; ++t) issue(t);
+  if (PIPE) {
+    __builtin_amdgcn_s_waitcnt(attn_wait_vm_lgkm0((R - 2) * PW));
     __builtin_amdgcn_s_barrier();
-    issue(grp + kRing, gslot);
-    gslot = gslot + 1 == kRing ? 0 : gslot + 1;
+    bf16x8 kf[2][4];
+    load_k(smem, kf);
+    mfma_scores(kf, sacc[0]);
+  }
+
+  // Key tile g: the tile needed now (g + 1 with read-ahead, else g) was issued in an
+  // earlier iteration or the prologue, and the DMAs of R - 3 (R - 2) later tiles follow
+  // it, hence the vmcnt. After the barrier every wave is done with tile g - 1, whose
+  // slot takes tile g + R - 1. With read-ahead, the scores of tile g + 1 are taken in
+  // every iteration (after the last tile its slot holds a valid reload of the last
+  // tile; those scores go unused), and their MFMAs are interleaved with the
+  // exponentials of tile g.
+  for (int g0 = 0; g0 < ntiles; g0 += U) {
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int g = g0 + j;
+      if (g < ntiles) {
+        __builtin_amdgcn_s_waitcnt(attn_wait_vm_lgkm0((PIPE ? R - 3 : R - 2) * PW));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue((j + R - 1) % R);
+        const unsigned char* Tg = smem + (j % R) * TILE;
+        bf16x8 kf[2][4], vf[2][2][2];
+        if (PIPE) {
+          load_k(smem + ((j + 1) % R) * TILE, kf);
+          load_v(Tg, vf);
+          softmax_max(g * kKT, sacc[j & 1]);
+          mfma_scores(kf, sacc[(j + 1) & 1]);
+          softmax_pv(sacc[j & 1], vf);
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // six VALU
+          }
+        } else {
+          load_k(Tg, kf);
+          load_v(Tg, vf);
+          mfma_scores(kf, sacc[0]);
+          softmax_max(g * kKT, sacc[0]);
+          softmax_pv(sacc[0], vf);
+        }
+      }
+    }
   }
   __builtin_amdgcn_s_waitcnt(attn_wait_vm_lgkm0(0));
-  __builtin_amdgcn_s_barrier();
-
-  // ---- merge the NK partial states of each query group (slots reused as scratch:
-  // per wave 64 lanes x 34 floats)
-  float* xch = reinterpret_cast<float*>(smem);
-  if (NK > 1) {
-    if (wk > 0) {
-      float* dst = xch + ((wk - 1) * NQ + wq) * 64 * 34 + lane;
-#pragma unroll
-      for (int d = 0; d < 2; ++d)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) dst[(d * 16 + r) * 64] = o[d][r];
-      dst[32 * 64] = m_ref;
-      dst[33 * 64] = l_run;
-    }
-    __syncthreads();
-    if (wk == 0) {
-#pragma unroll
-      for (int k = 1; k < NK; ++k) {
-        const float* src = xch + ((k - 1) * NQ + wq) * 64 * 34 + lane;
-        const float m2 = src[32 * 64], l2 = src[33 * 64];
-        const float m_new = fmaxf(m_ref, m2);
-        const float a1 = m_ref == -INFINITY ? 0.f : fast_exp2(m_ref - m_new);
-        const float a2 = m2 == -INFINITY ? 0.f : fast_exp2(m2 - m_new);
-        l_run = l_run * a1 + l2 * a2;
-#pragma unroll
-        for (int d = 0; d < 2; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[d][r] = o[d][r] * a1 + src[(d * 16 + r) * 64] * a2;
-        m_ref = m_new;
-      }
-    }
-  }
 
   const int qi = q0 + (lane & 31);
-  if (wk == 0 && qi < p.Sq) {
+  if (qi < p.Sq) {
     const float inv = 1.f / l_run;
     bf16* op = static_cast<bf16*>(p.o) + b * p.o_bs + (long long)qi * p.ldo + h * D;
 #pragma unroll
@@ -493,17 +521,17 @@ __global__ __launch_bounds__(64 * NQ * NK) void attn_dma_kernel(AttnParams p, in
   }
 }
 
-template <int NQ, int NK> void launch_dma(const AttnParams& p, hipStream_t s) {
-  constexpr int TILE = 2 * kKT * 128;
-  const size_t lds = std::max(size_t(kRing) * NK * TILE, size_t(NK - 1) * NQ * 64 * 34 * 4);
+template <int NQ, int R, int WPE, bool PIPE> void launch_pipe(const AttnParams& p, hipStream_t s) {
+  constexpr size_t lds = size_t(R) * 2 * kKT * 128;
   static bool attr_set = false;
   if (!attr_set) {
-    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_dma_kernel<NQ, NK>),
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_pipe_kernel<NQ, R, WPE, PIPE>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
     attr_set = true;
   }
   const int qtiles = (p.Sq + 32 * NQ - 1) / (32 * NQ);
-  hipLaunchKernelGGL((attn_dma_kernel<NQ, NK>), dim3(qtiles * p.heads * p.B), dim3(64 * NQ * NK), lds, s, p, qtiles);
+  hipLaunchKernelGGL((attn_pipe_kernel<NQ, R, WPE, PIPE>), dim3(qtiles * p.heads * p.B), dim3(64 * NQ), lds, s, p,
+                     qtiles);
 }
 
 template <typename T, int D, int NW> void launch(dim3 grid, const AttnParams& p, hipStream_t s) {
@@ -527,15 +555,11 @@ template <typename T> void attention(const AttnParams& p, int D, hipStream_t s) 
   constexpr int VEC = 16 / sizeof(T);
   DN_CHECK(p.ldq % VEC == 0 && p.ldk % VEC == 0 && p.vt_ld % VEC == 0, "attention: strides must be 16-byte multiples");
   DN_CHECK(p.vt_ld >= (p.Skv + kKT - 1) / kKT * kKT, "attention: V^T rows must cover whole 64-key tiles");
-  // bf16 self-attention over long key ranges: the direct-to-LDS kernel with the key
-  // range split over two wave groups (4 x 32 queries per workgroup for long query
-  // ranges, 2 x 32 otherwise); short key ranges (cross-attention) keep the
-  // register-staged kernel below, whose single pass has no merge step.
+  // bf16 attention over long key ranges (self-attention): the software-pipelined
+  // kernel, 4 x 32 queries per workgroup, a ring of 3 key tiles, score read-ahead.
+  // Short key ranges (cross-attention) keep the register-staged kernel below.
   if (sizeof(T) == 2 && D == 64 && p.Skv >= 256) {
-    if (p.Sq >= 2048)
-      launch_dma<4, 2>(p, s);
-    else
-      launch_dma<2, 2>(p, s);
+    launch_pipe<4, 3, 2, true>(p, s);
     DN_HIP(hipGetLastError());
     return;
   }
