@@ -245,6 +245,10 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnParams p) {
 //    takes tile g's row maximum, then issues the S^T = K Q^T MFMAs of tile g + 1
 //    interleaved with the exponentials of tile g, and O^T += V^T P^T for tile g;
 //    without: scores and softmax of tile g in turn.
+// Q enters the MFMAs multiplied by scale * log2(e) (rounded to bf16), and the score
+// accumulators start from minus the reference maximum of the lane's query, so the
+// MFMAs produce the base-2 exponent directly (the first tile starts from zero; a move
+// of the reference shifts the current tile's scores by the difference).
 // Within each 16-key group the K tile holds its keys in the order of bit 2 and bit 3
 // of the key index swapped: score register 8c + e of a 32-key block then belongs to
 // key 16c + 8h + e (h = lane half), so the V^T operand of a P fragment is 8
@@ -286,12 +290,16 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
   const bf16* kp = static_cast<const bf16*>(p.k) + b * p.k_bs + h * D;
   const bf16* vtp = static_cast<const bf16*>(p.vt) + ((long long)b * p.heads + h) * D * p.vt_ld;
 
+  // Q times scale * log2(e), rounded to bf16: the MFMAs then produce base-2 logits
   bf16x8 qf[4];
   {
     const int qrow = min(q0 + (lane & 31), p.Sq - 1);
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      qf[s] = *reinterpret_cast<const bf16x8*>(qp + (long long)qrow * p.ldq + s * 16 + half * 8);
+    for (int s = 0; s < 4; ++s) {
+      const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + (long long)qrow * p.ldq + s * 16 + half * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[s][e] = static_cast<bf16>(static_cast<float>(raw[e]) * p.scale_log2);
+    }
   }
 
   // DMA: instruction i = wave * PW + j of a tile fills rows [8 i, 8 i + 8) of its ring
@@ -364,11 +372,11 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
 #pragma unroll
         for (int c = 0; c < 2; ++c) vf[d][kb][c] = *reinterpret_cast<const bf16x8*>(T + d * 32 * ROWB + voff[kb][c]);
   };
-  // S^T = K Q^T for the 64 keys of a tile (two 32-key blocks)
-  auto mfma_scores = [&](const bf16x8 (&kf)[2][4], f32x16* sa) {
-    const f32x16 zero = {};
+  // S^T = K Q^T - m for the 64 keys of a tile (two 32-key blocks): the accumulators
+  // start from c0, the negated reference maximum of the lane's query (or zero)
+  auto mfma_scores = [&](const bf16x8 (&kf)[2][4], f32x16* sa, const f32x16& c0) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sa[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb][0], qf[0], zero, 0, 0, 0);
+    for (int kb = 0; kb < 2; ++kb) sa[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb][0], qf[0], c0, 0, 0, 0);
 #pragma unroll
     for (int s2 = 1; s2 < 4; ++s2)
 #pragma unroll
@@ -383,6 +391,11 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
     for (int r = 0; r < 16; ++r) o[d][r] = 0.f;
   float m_ref = -INFINITY, l_run = 0.f;
   f32x16 sacc[2][2];
+  // -m_ref in all 16 registers: the start value of the next tile's score accumulators,
+  // which then hold base-2 logits minus the reference maximum
+  f32x16 negm;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) negm[r] = 0.f;
 
   // value of x in lane l ^ 32 (lanes l and l ^ 32 hold one query's two key halves)
   auto partner = [](float x) {
@@ -392,8 +405,10 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
   };
 
   // softmax, first part: key padding of the last tile, the tile's row maximum, and a
-  // move of the reference maximum (rescaling O and l) when it grew by more than kLazy
-  auto softmax_max = [&](int k0, f32x16* sa) {
+  // move of the reference maximum (rescaling O and l) when it grew by more than kLazy.
+  // The tile's scores hold logit - m_fold (m_fold = m_ref when they were computed, 0 for
+  // the first tile); on a move they are shifted to the new reference.
+  auto softmax_max = [&](int k0, f32x16* sa, float m_fold) {
     if (k0 + kKT > p.Skv) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -410,7 +425,7 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
       mc[j] = fmaxf(m, sa[1][4 * j + 3]);
     }
     float mx = fmaxf(fmaxf(mc[0], mc[1]), fmaxf(mc[2], mc[3]));
-    mx = fmaxf(mx, partner(mx)) * p.scale_log2;
+    mx = fmaxf(mx, partner(mx)) + m_fold;
     if (__any(mx > m_ref + kLazy)) {
       const float m_new = fmaxf(m_ref, mx);
       const float alpha = fast_exp2(m_ref - m_new);
@@ -419,7 +434,14 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
       for (int d = 0; d < 2; ++d)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+      const float shift = m_new - m_fold;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sa[kb][r] -= shift;
       m_ref = m_new;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) negm[r] = -m_new;
     }
   };
   // softmax, second part: P = 2^(s scale - m) in bf16, its row sum, O^T += V^T P^T
@@ -433,7 +455,7 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
       for (int c = 0; c < 2; ++c) {
         bf16x8 pv;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pv[e] = static_cast<bf16>(fast_exp2(sa[kb][8 * c + e] * p.scale_log2 - m_ref));
+        for (int e = 0; e < 8; ++e) pv[e] = static_cast<bf16>(fast_exp2(sa[kb][8 * c + e]));
         pf[kb][c] = pv;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -461,7 +483,7 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
     __builtin_amdgcn_s_barrier();
     bf16x8 kf[2][4];
     load_k(smem, kf);
-    mfma_scores(kf, sacc[0]);
+    mfma_scores(kf, sacc[0], negm);
   }
 
   // Key tile g: the tile needed now (g + 1 with read-ahead, else g) was issued in an
@@ -485,8 +507,8 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
         if (PIPE) {
           load_k(smem + ((j + 1) % R) * TILE, kf);
           load_v(Tg, vf);
-          softmax_max(g * kKT, sacc[j & 1]);
-          mfma_scores(kf, sacc[(j + 1) & 1]);
+          softmax_max(g * kKT, sacc[j & 1], g == 0 ? 0.f : m_ref);
+          mfma_scores(kf, sacc[(j + 1) & 1], negm);
           softmax_pv(sacc[j & 1], vf);
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
@@ -495,9 +517,10 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
           }
         } else {
           load_k(Tg, kf);
+          const float m_fold = g == 0 ? 0.f : m_ref;
+          mfma_scores(kf, sacc[0], negm);
+          softmax_max(g * kKT, sacc[0], m_fold);
           load_v(Tg, vf);
-          mfma_scores(kf, sacc[0]);
-          softmax_max(g * kKT, sacc[0]);
           softmax_pv(sacc[0], vf);
         }
       }
@@ -556,10 +579,15 @@ template <typename T> void attention(const AttnParams& p, int D, hipStream_t s) 
   DN_CHECK(p.ldq % VEC == 0 && p.ldk % VEC == 0 && p.vt_ld % VEC == 0, "attention: strides must be 16-byte multiples");
   DN_CHECK(p.vt_ld >= (p.Skv + kKT - 1) / kKT * kKT, "attention: V^T rows must cover whole 64-key tiles");
   // bf16 attention over long key ranges (self-attention): the software-pipelined
-  // kernel, 4 x 32 queries per workgroup, a ring of 3 key tiles, score read-ahead.
-  // Short key ranges (cross-attention) keep the register-staged kernel below.
+  // kernel with a ring of 3 key tiles; long query ranges: 4 x 32 queries per workgroup
+  // at three waves per SIMD without score read-ahead, otherwise 2 x 32 queries with
+  // read-ahead (the faster of the measured shapes at 4096 and 1024 tokens). Short key
+  // ranges (cross-attention) keep the register-staged kernel below.
   if (sizeof(T) == 2 && D == 64 && p.Skv >= 256) {
-    launch_pipe<4, 3, 2, true>(p, s);
+    if (p.Sq >= 2048)
+      launch_pipe<4, 3, 3, false>(p, s);
+    else
+      launch_pipe<2, 3, 2, true>(p, s);
     DN_HIP(hipGetLastError());
     return;
   }
