@@ -376,7 +376,7 @@ dn_status dn_op_groupnorm(int32_t dtype, const void* x, void* y, int32_t n, int3
     DN_CHECK(x && y && gamma && beta, "dn_op_groupnorm: null pointer");
     DN_CHECK(n >= 1 && HW >= 1 && C >= 1 && G >= 1 && C % G == 0, "dn_op_groupnorm: bad sizes");
     float* ws = nullptr;
-    const size_t part = dn::groupnorm_workspace_floats(n, HW, C);
+    const size_t part = dn::groupnorm_workspace_floats(n, HW, C, G);
     DN_HIP(hipMalloc(&ws, (part + (size_t)2 * n * C) * 4));
     try {
       dn::GroupNormParams p;

@@ -114,7 +114,7 @@ struct GroupNormParams {
   float* partial = nullptr;  // workspace, groupnorm_workspace_floats()
   float* stats = nullptr;    // workspace [2][n][C]: per-channel scale, then shift
 };
-size_t groupnorm_workspace_floats(int n, int HW, int C);
+size_t groupnorm_workspace_floats(int n, int HW, int C, int G);
 template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s);
 
 template <typename T>

@@ -559,7 +559,7 @@ void size_workspace(Model* m, Sizer& z) {
   std::vector<int> skipc;
   auto gn = [&](int HW, int C) {
     z.gn_out = std::max(z.gn_out, (size_t)n * HW * C);
-    z.gn_partial = std::max(z.gn_partial, groupnorm_workspace_floats(n, HW, C));
+    z.gn_partial = std::max(z.gn_partial, groupnorm_workspace_floats(n, HW, C, m->cfg.gn_groups));
     z.gn_stats = std::max(z.gn_stats, (size_t)2 * n * C);
   };
   m->act_h.clear();

@@ -1,11 +1,13 @@
 // GroupNorm (+SiLU) and LayerNorm kernels (HBM-bound; gfx950).
 //
 // GroupNorm on NHWC activations runs in three launches:
-//   1. partial: each workgroup reduces a chunk of pixels of one sample into
-//      per-channel fp32 sums of x and x^2 (16-byte coalesced loads; a thread
-//      owns one 16-byte channel vector, so its accumulators never mix channels);
-//   2. finalize: one workgroup per (sample, group) merges the chunk partials in
-//      fp64 in a fixed order and writes per-(sample, channel) scale and shift
+//   1. partial: each workgroup reduces a chunk of pixels of one sample and a slice of
+//      up to 256 channel vectors into fp32 sums of x and x^2 per group (16-byte
+//      coalesced loads; a thread owns one 16-byte channel vector, so its accumulators
+//      never mix channels; per-channel sums meet in LDS, then one thread per group adds
+//      the group's channels in that slice, zero for groups outside it);
+//   2. finalize: one workgroup per (sample, group) merges the (chunk, slice) partials
+//      in fp64 in a fixed order and writes per-(sample, channel) scale and shift
 //      (gamma * rstd, beta - mean * gamma * rstd);
 //   3. apply: y = x * scale + shift (then SiLU), one FMA per element, 16-byte
 //      vectors, a (pixel block, sample) grid.
@@ -19,7 +21,7 @@
 namespace dn {
 namespace {
 
-constexpr int kPixPerThread = 32;
+constexpr int kPixPerThread = 8;
 
 struct GnGeom {
   int C, V, vslices, chunks, pix_per_chunk;
@@ -87,14 +89,28 @@ __global__ __launch_bounds__(256) void gn_partial_kernel(GroupNormParams p, GnGe
     }
   }
   __syncthreads();
-  for (int j = tid; j < vz * VEC; j += 256) {
+  // per-channel sums over the pixel lanes (in place, lane 0's slots), then per group
+  const int nch = vz * VEC;
+  for (int j = tid; j < nch; j += 256) {
     float ss = 0.f, qq = 0.f;
     for (int l = 0; l < pl_count; ++l) {
-      ss += red[(l * vz * VEC + j) * 2 + 0];
-      qq += red[(l * vz * VEC + j) * 2 + 1];
+      ss += red[(l * nch + j) * 2 + 0];
+      qq += red[(l * nch + j) * 2 + 1];
     }
-    const int c = v_begin * VEC + j;
-    float* out = p.partial + (((long long)n * g.chunks + chunk) * g.C + c) * 2;
+    red[j * 2 + 0] = ss;
+    red[j * 2 + 1] = qq;
+  }
+  __syncthreads();
+  const int cg = g.C / p.G;
+  const int c_begin = v_begin * VEC;
+  for (int grp = tid; grp < p.G; grp += 256) {
+    const int lo = max(grp * cg, c_begin) - c_begin, hi = min((grp + 1) * cg, c_begin + nch) - c_begin;
+    float ss = 0.f, qq = 0.f;
+    for (int j = lo; j < hi; ++j) {
+      ss += red[j * 2 + 0];
+      qq += red[j * 2 + 1];
+    }
+    float* out = p.partial + ((((long long)n * g.chunks + chunk) * g.vslices + z) * p.G + grp) * 2;
     out[0] = ss;
     out[1] = qq;
   }
@@ -105,11 +121,10 @@ __global__ __launch_bounds__(256) void gn_finalize_kernel(GroupNormParams p, GnG
   const int tid = threadIdx.x;
   const int grp = blockIdx.x, n = blockIdx.y;
   const int cg = g.C / p.G;
-  const int items = g.chunks * cg;
+  const int items = g.chunks * g.vslices;
   double s = 0.0, q = 0.0;
   for (int i = tid; i < items; i += 256) {
-    const int chunk = i / cg, c = grp * cg + (i - chunk * cg);
-    const float* in = p.partial + (((long long)n * g.chunks + chunk) * g.C + c) * 2;
+    const float* in = p.partial + (((long long)n * items + i) * p.G + grp) * 2;
     s += in[0];
     q += in[1];
   }
@@ -277,12 +292,12 @@ __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, in
 
 }  // namespace
 
-size_t groupnorm_workspace_floats(int n, int HW, int C) {
-  // Sized for the smaller vector width (fp32 -> 4 channels per vector -> more pixel lanes).
+size_t groupnorm_workspace_floats(int n, int HW, int C, int G) {
+  // [n][chunk][slice][G] (sum, sum of squares); the larger of the fp32 and bf16 geometries
   const GnGeom g = gn_geom<float>(HW, C);
   const GnGeom g2 = gn_geom<bf16>(HW, C);
-  const int chunks = g.chunks > g2.chunks ? g.chunks : g2.chunks;
-  return size_t(n) * chunks * C * 2;
+  const size_t a = size_t(g.chunks) * g.vslices, b = size_t(g2.chunks) * g2.vslices;
+  return size_t(n) * (a > b ? a : b) * G * 2;
 }
 
 template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s) {
