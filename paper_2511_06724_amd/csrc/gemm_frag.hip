@@ -45,6 +45,19 @@ typedef __attribute__((address_space(1))) void gbl_void;
 // expcnt unconstrained (bits 6:4 = 7).
 constexpr int wait_vm_lgkm0(int vm) { return (vm & 0xF) | (((vm >> 4) & 3) << 14) | (7 << 4); }
 
+// 16 bytes per lane global -> LDS (lane i writes lds + 16 i). Issued from inline
+// assembly: the compiler's wait insertion treats a global_load_lds it knows about as
+// making the vector-memory counter out of order and then drains every load
+// (vmcnt(0)) before the next use of any loaded register, which would serialise the
+// B-register prefetch with every A stage. The LDS data this writes is guarded by the
+// kernel's own waits and barriers (hand-overs, and a full drain before the epilogue);
+// it writes no VGPRs. M0 holds the LDS address; nothing else in these kernels keeps a
+// value in M0.
+__device__ __forceinline__ void dma16(const void* g, lds_void* lds) {
+  const unsigned a = static_cast<unsigned>(reinterpret_cast<__UINTPTR_TYPE__>(lds));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(a) : "memory", "m0");
+}
+
 // Scheduling-group pattern of one k-step: NM MFMAs, each followed by one LDS read
 // (while the NR reads last) and by its share of the NV B loads.
 template <int I, int NM, int NR, int NV> struct KSched {
@@ -183,7 +196,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
         g = a_src + ((MODE == 1 && second) ? off1[j] : off0[j]) + a_c;
       }
       if (!real) g = static_cast<const bf16*>(p.zero16);
-      __builtin_amdgcn_global_load_lds((gbl_void*)g, (lds_void*)(stage + q * 1024), 16, 0, 0);
+      dma16(g, (lds_void*)(stage + q * 1024));
     }
   };
 
@@ -274,7 +287,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
         mfmas(cur[s], bb[s]);
         load_b_step(kt + D, s, bb);
       }
-      if (r >= 1) __builtin_amdgcn_sched_group_barrier(0x020, PW, 0);
       KSched<0, 4 * NM, 4 * FM, 4 * FN>::apply();
       __builtin_amdgcn_sched_barrier(0);
     };
@@ -300,7 +312,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
       read_a(rd_slot, rd_s, a_next);
       mfmas(a_use, b_use);
       load_b_step(bkt, s, bb);
-      if constexpr (decltype(dma)::value) __builtin_amdgcn_sched_group_barrier(0x020, PW, 0);
       KSched<0, NM, FM, FN>::apply();
       __builtin_amdgcn_sched_barrier(0);
     };
@@ -392,7 +403,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
         *reinterpret_cast<f32x4*>(ep + col * EPL + j * 32 + 8 * g + h4) =
             f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
     const int mb = m0 + i * 32;
-    if (SPLIT || !p.geglu) {
+    if (SPLIT) {
       constexpr int LPR = WN / 4;   // lanes per row
       constexpr int RPI = 64 / LPR; // rows per pass
 #pragma unroll
@@ -402,35 +413,106 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
         const f32x4 v4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c4);
         const int m = mb + rr, n = nw0 + c4;
         if (m >= p.M || n >= p.n_store) continue;
-        if (SPLIT) {
-          *reinterpret_cast<f32x4*>(slab + (long long)m * p.n_store + n) = v4;
-        } else {
-          float v[4] = {v4[0], v4[1], v4[2], v4[3]};
-          epilogue_group<bf16>(p, m, n, v);
+        *reinterpret_cast<f32x4*>(slab + (long long)m * p.n_store + n) = v4;
+      }
+    } else if (!p.geglu) {
+      // A lane's 4 columns are the same in every pass; the row vector and residual of
+      // every pass of this 32-row block are loaded before the block is read back from
+      // LDS, so the block waits on one memory latency instead of one per pass. Same
+      // arithmetic as epilogue_group: ((acc + bias) + row vector) + residual.
+      constexpr int LPR = WN / 4;
+      constexpr int RPI = 64 / LPR;
+      constexpr int NP = 32 / RPI;
+      const int c4 = (lane % LPR) * 4;
+      const int n = nw0 + c4;
+      const bool ncol = n < p.n_store;
+      const bool full = n + 4 <= p.n_store;
+      float rv[NP][4], rs[NP][4];
+#pragma unroll
+      for (int t = 0; t < NP; ++t) {
+        const int m = mb + t * RPI + lane / LPR;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rv[t][e] = rs[t][e] = 0.f;
+        if (m >= p.M || !ncol) continue;
+        if (p.rowvec) {
+          const float* r = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) rv[t][e] = (full || n + e < p.n_store) ? r[e] : 0.f;
         }
+        if (p.resid) {
+          const long long ro = (long long)m * p.ldr + n;
+          if (full && (p.ldr & 3) == 0) {
+            if (p.resid_f32) {
+              const f32x4 r = *reinterpret_cast<const f32x4*>(static_cast<const float*>(p.resid) + ro);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) rs[t][e] = r[e];
+            } else {
+              const bf16x4 r = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(p.resid) + ro);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) rs[t][e] = static_cast<float>(r[e]);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (n + e < p.n_store)
+                rs[t][e] = p.resid_f32 ? static_cast<const float*>(p.resid)[ro + e]
+                                       : static_cast<float>(static_cast<const bf16*>(p.resid)[ro + e]);
+          }
+        }
+      }
+      float bias4[4] = {0.f, 0.f, 0.f, 0.f};
+      if (p.bias && ncol) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bias4[e] = (full || n + e < p.n_store) ? p.bias[n + e] : 0.f;
+      }
+#pragma unroll
+      for (int t = 0; t < NP; ++t) {
+        const int rr = t * RPI + lane / LPR;
+        const f32x4 v4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c4);
+        const int m = mb + rr;
+        if (m >= p.M || !ncol) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float x = v4[e];
+          if (p.bias) x += bias4[e];
+          if (p.rowvec) x += rv[t][e];
+          if (p.resid) x += rs[t][e];
+          v[e] = x;
+        }
+        store4<bf16>(p, m, n, v, p.n_store);
       }
     } else {
       // GEGLU: within each 64-column pair block, columns [0, 32) are values and
-      // [32, 64) the matching gates; output column = (pair block) * 32 + c
+      // [32, 64) the matching gates; output column = (pair block) * 32 + c. A lane's
+      // value and gate columns are the same in every pass: their biases load once.
       constexpr int LPR = WN / 8;
       constexpr int RPI = 64 / LPR;
+      const int cq = (lane % LPR) * 4;            // 0 .. WN/2 - 4
+      const int pb = cq / 32, c4 = cq % 32;       // pair block, column in it
+      const int lc = pb * 64 + c4;                // value column within the wave
+      const int nv = nw0 + lc;
+      const int o = nw0 / 2 + cq;
+      float ba[4] = {0.f, 0.f, 0.f, 0.f}, bg[4] = {0.f, 0.f, 0.f, 0.f};
+      if (p.bias && o < p.n_store) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          ba[e] = p.bias[nv + e];
+          bg[e] = p.bias[nv + 32 + e];
+        }
+      }
 #pragma unroll
       for (int t = 0; t < 32 / RPI; ++t) {
         const int rr = t * RPI + lane / LPR;
-        const int cq = (lane % LPR) * 4;            // 0 .. WN/2 - 4
-        const int pb = cq / 32, c4 = cq % 32;       // pair block, column in it
-        const int lc = pb * 64 + c4;                // value column within the wave
         const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc);
         const f32x4 g4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 32);
         const int m = mb + rr;
-        const int nv = nw0 + lc;
-        const int o = nw0 / 2 + cq;
         if (m >= p.M || o >= p.n_store) continue;
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float a = a4[e] + (p.bias ? p.bias[nv + e] : 0.f);
-          const float gg = g4[e] + (p.bias ? p.bias[nv + 32 + e] : 0.f);
+          const float a = a4[e] + ba[e];
+          const float gg = g4[e] + bg[e];
           v[e] = a * gelu_erf(gg);
         }
         store4<bf16>(p, m, o, v, p.n_store);
