@@ -225,6 +225,57 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // Epilogue input of the plain path (the residual or the per-sample row vector, when
+  // exactly one is present) for small wave tiles of the linear modes without stage
+  // read-ahead (where the registers are free): loaded before the main loop, whose
+  // latency then hides the load, into FM x ENP 16-byte registers per lane.
+  constexpr int ELPR = WN / 4;     // lanes per row in the row-contiguous epilogue
+  constexpr int ERPI = 64 / ELPR;  // rows per pass
+  constexpr int ENP = 32 / ERPI;   // passes per 32-row block
+  constexpr bool kPreIn = !SPLIT && !PRE && MODE != 2 && FM * ENP * 4 <= 32;
+  const int enw0 = n0 + wave * WN;
+  const bool pre_in = kPreIn && !p.geglu && !(p.vt && enw0 + WN > p.vt_col0) &&
+                      ((p.resid != nullptr) != (p.rowvec != nullptr));
+  f32x4 pin[kPreIn ? FM : 1][kPreIn ? ENP : 1];
+  if constexpr (kPreIn) {
+    if (pre_in) {
+      const int n = enw0 + (lane % ELPR) * 4;
+      const bool full = n + 4 <= p.n_store;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int t = 0; t < ENP; ++t) {
+          const int m = m0 + i * 32 + t * ERPI + lane / ELPR;
+          f32x4 v = {0.f, 0.f, 0.f, 0.f};
+          if (m < p.M && n < p.n_store) {
+            if (p.rowvec) {
+              const float* r = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = (full || n + e < p.n_store) ? r[e] : 0.f;
+            } else {
+              const long long ro = (long long)m * p.ldr + n;
+              if (full && (p.ldr & 3) == 0) {
+                if (p.resid_f32) {
+                  v = *reinterpret_cast<const f32x4*>(static_cast<const float*>(p.resid) + ro);
+                } else {
+                  const bf16x4 r = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(p.resid) + ro);
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) v[e] = static_cast<float>(r[e]);
+                }
+              } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  if (n + e < p.n_store)
+                    v[e] = p.resid_f32 ? static_cast<const float*>(p.resid)[ro + e]
+                                       : static_cast<float>(static_cast<const bf16*>(p.resid)[ro + e]);
+              }
+            }
+          }
+          pin[i][t] = v;
+        }
+    }
+  }
+
   // A fragment of k-step s: row (lane % 32) of each 32-row block, logical chunk
   // 2 s + (lane / 32) at its swizzled position.
   const int frow = lane & 31;
@@ -433,7 +484,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
         const int m = mb + t * RPI + lane / LPR;
 #pragma unroll
         for (int e = 0; e < 4; ++e) rv[t][e] = rs[t][e] = 0.f;
-        if (m >= p.M || !ncol) continue;
+        if (m >= p.M || !ncol || pre_in) continue;
         if (p.rowvec) {
           const float* r = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
 #pragma unroll
@@ -476,8 +527,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
         for (int e = 0; e < 4; ++e) {
           float x = v4[e];
           if (p.bias) x += bias4[e];
-          if (p.rowvec) x += rv[t][e];
-          if (p.resid) x += rs[t][e];
+          if constexpr (kPreIn) {
+            if (pre_in) x += pin[i][t][e];
+          }
+          if (!pre_in) {
+            if (p.rowvec) x += rv[t][e];
+            if (p.resid) x += rs[t][e];
+          }
           v[e] = x;
         }
         store4<bf16>(p, m, n, v, p.n_store);
