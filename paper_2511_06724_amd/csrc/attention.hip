@@ -578,13 +578,16 @@ template <typename T> void attention(const AttnParams& p, int D, hipStream_t s) 
   constexpr int VEC = 16 / sizeof(T);
   DN_CHECK(p.ldq % VEC == 0 && p.ldk % VEC == 0 && p.vt_ld % VEC == 0, "attention: strides must be 16-byte multiples");
   DN_CHECK(p.vt_ld >= (p.Skv + kKT - 1) / kKT * kKT, "attention: V^T rows must cover whole 64-key tiles");
-  // bf16 attention over long key ranges (self-attention): the software-pipelined
-  // kernel with a ring of 3 key tiles; long query ranges: 4 x 32 queries per workgroup
-  // at three waves per SIMD without score read-ahead, otherwise 2 x 32 queries with
-  // read-ahead (the faster of the measured shapes at 4096 and 1024 tokens). Short key
-  // ranges (cross-attention) keep the register-staged kernel below.
-  if (sizeof(T) == 2 && D == 64 && p.Skv >= 256) {
-    if (p.Sq >= 2048)
+  // bf16, head dim 64: the software-pipelined kernel. Long key ranges (self-attention)
+  // use a ring of 3 key tiles; long query ranges: 4 x 32 queries per workgroup at three
+  // waves per SIMD without score read-ahead, otherwise 2 x 32 queries with read-ahead.
+  // Short key ranges (cross-attention over the 77 text tokens) use a ring of 2 tiles,
+  // 4 x 32 queries, three waves per SIMD (the fastest measured shapes for 4096 and
+  // 1024 tokens). fp32 and head dim 32 take the register-staged kernel below.
+  if (sizeof(T) == 2 && D == 64) {
+    if (p.Skv < 256)
+      launch_pipe<4, 2, 3, false>(p, s);
+    else if (p.Sq >= 2048)
       launch_pipe<4, 3, 3, false>(p, s);
     else
       launch_pipe<2, 3, 2, true>(p, s);
