@@ -221,48 +221,66 @@ template <> struct Store4<float> {
   }
 };
 
-// One wave per row. With nsplit > 0 the row is first rebuilt from the residual stream:
+// One wave per row. With NS > 0 the row is first rebuilt from the residual stream:
 // x[row] = (resid ? x[row] : 0) + bias + sum_s part[s][row] in that order (the reduction of
 // a split-K GEMM that wrote fp32 partial slabs), and written back; then
-// y = (x - mean) * rstd * gamma + beta with two-pass mean / variance.
-template <typename T>
+// y = (x - mean) * rstd * gamma + beta with two-pass mean / variance. Every load of the
+// row (x, the slabs, the bias) is issued before the first use, so a row waits on one
+// memory latency; vector columns past C are skipped wave-uniformly, lanes past C read a
+// valid column and are masked.
+template <typename T, int NS>
 __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, int C, const float* gamma,
-                                                 const float* beta, float eps, const float* part, int nsplit,
-                                                 long long slab, const float* bias, int resid) {
+                                                 const float* beta, float eps, const float* part, long long slab,
+                                                 const float* bias, int resid) {
   const int lane = threadIdx.x & 63;
   const long long row = blockIdx.x * 4ll + (threadIdx.x >> 6);
   if (row >= M) return;
   const int nv = C / 4;
   float4* xr = reinterpret_cast<float4*>(x + row * C);
+  const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
   float4 v[kLnMaxVec];
+  float4 sl[NS > 0 ? NS : 1][kLnMaxVec];
+  float4 bv[kLnMaxVec];
+#pragma unroll
+  for (int j = 0; j < kLnMaxVec; ++j) {
+    v[j] = bv[j] = zero4;
+#pragma unroll
+    for (int k = 0; k < (NS > 0 ? NS : 1); ++k) sl[k][j] = zero4;
+    if (64 * j < nv) {
+      const int i = min(lane + 64 * j, nv - 1);
+      if (NS == 0 || resid) v[j] = xr[i];
+      if constexpr (NS > 0) {
+        if (bias) bv[j] = reinterpret_cast<const float4*>(bias)[i];
+        const float4* pr = reinterpret_cast<const float4*>(part + row * C);
+#pragma unroll
+        for (int k = 0; k < NS; ++k) sl[k][j] = pr[k * (slab / 4) + i];
+      }
+    }
+  }
   float s = 0.f;
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
     const int i = lane + 64 * j;
-    if (i < nv) {
-      if (nsplit > 0) {
-        float4 a = resid ? xr[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (64 * j < nv) {
+      if constexpr (NS > 0) {
+        float4 a = v[j];
         if (bias) {
-          const float4 b = reinterpret_cast<const float4*>(bias)[i];
-          a.x += b.x;
-          a.y += b.y;
-          a.z += b.z;
-          a.w += b.w;
+          a.x += bv[j].x;
+          a.y += bv[j].y;
+          a.z += bv[j].z;
+          a.w += bv[j].w;
         }
-        const float4* pr = reinterpret_cast<const float4*>(part + row * C);
-        for (int k = 0; k < nsplit; ++k) {
-          const float4 t = pr[k * (slab / 4) + i];
-          a.x += t.x;
-          a.y += t.y;
-          a.z += t.z;
-          a.w += t.w;
+#pragma unroll
+        for (int k = 0; k < NS; ++k) {
+          a.x += sl[k][j].x;
+          a.y += sl[k][j].y;
+          a.z += sl[k][j].z;
+          a.w += sl[k][j].w;
         }
-        xr[i] = a;
         v[j] = a;
-      } else {
-        v[j] = xr[i];
+        if (i < nv) xr[i] = a;
       }
-      s += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+      if (i < nv) s += (v[j].x + v[j].y) + (v[j].z + v[j].w);
     }
   }
   const float mean = wave_sum(s) / C;
@@ -270,7 +288,7 @@ __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, in
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
     const int i = lane + 64 * j;
-    if (i < nv) {
+    if (64 * j < nv && i < nv) {
       const float a = v[j].x - mean, b = v[j].y - mean, c = v[j].z - mean, d = v[j].w - mean;
       q += (a * a + b * b) + (c * c + d * d);
     }
@@ -282,12 +300,19 @@ __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, in
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
     const int i = lane + 64 * j;
-    if (i < nv) {
+    if (64 * j < nv && i < nv) {
       const float4 g = g4[i], bb = b4[i];
       Store4<T>::st(yr + 4 * i, (v[j].x - mean) * rstd * g.x + bb.x, (v[j].y - mean) * rstd * g.y + bb.y,
                     (v[j].z - mean) * rstd * g.z + bb.z, (v[j].w - mean) * rstd * g.w + bb.w);
     }
   }
+}
+
+template <typename T, int NS>
+void launch_ln(float* x, T* y, long long M, int C, const float* gamma, const float* beta, float eps, const float* part,
+               const float* bias, bool resid, hipStream_t s) {
+  hipLaunchKernelGGL((ln_kernel<T, NS>), dim3(static_cast<unsigned>((M + 3) / 4)), dim3(256), 0, s, x, y, M, C, gamma,
+                     beta, eps, part, M * C, bias, resid ? 1 : 0);
 }
 
 }  // namespace
@@ -330,8 +355,18 @@ void layernorm_reduce(float* x, T* y, long long M, int C, const float* gamma, co
                (uintptr_t)y % (4 * sizeof(T)) == 0,
            "layernorm: x, gamma, beta, partials and bias must be 16-byte aligned, y aligned to 4 elements");
   DN_CHECK(nsplit == 0 || part, "layernorm: partial slabs missing");
-  hipLaunchKernelGGL(ln_kernel<T>, dim3(static_cast<unsigned>((M + 3) / 4)), dim3(256), 0, s, x, y, M, C, gamma,
-                     beta, eps, part, nsplit, M * C, bias, resid ? 1 : 0);
+  switch (nsplit) {
+    case 0: launch_ln<T, 0>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 1: launch_ln<T, 1>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 2: launch_ln<T, 2>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 3: launch_ln<T, 3>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 4: launch_ln<T, 4>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 5: launch_ln<T, 5>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 6: launch_ln<T, 6>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 7: launch_ln<T, 7>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    case 8: launch_ln<T, 8>(x, y, M, C, gamma, beta, eps, part, bias, resid, s); break;
+    default: throw Error(-1, "layernorm: at most 8 partial slabs");
+  }
   DN_HIP(hipGetLastError());
 }
 
