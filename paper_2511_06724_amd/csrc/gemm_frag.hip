@@ -577,9 +577,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
   }
 }
 
-// Sum of the split-K partial slabs [nsplit][M][n_store] in split order, then the
-// epilogue; one thread per 4 consecutive columns of a row.
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, int nsplit) {
+// Sum of the split-K partial slabs [NS][M][n_store] in split order, then the epilogue;
+// one thread per 4 consecutive columns of a row, all slab loads issued before the sum.
+template <int NS> __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p) {
   const int q = p.n_store / 4;
   const long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x;
   if (i >= (long long)p.M * q) return;
@@ -587,16 +587,35 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, int ns
   const int n = (int)(i - (long long)m * q) * 4;
   const long long slab = (long long)p.M * p.n_store;
   const float* src = p.part + (long long)m * p.n_store + n;
-  f32x4 s = *reinterpret_cast<const f32x4*>(src);
-  for (int k = 1; k < nsplit; ++k) {
-    const f32x4 t = *reinterpret_cast<const f32x4*>(src + k * slab);
-    s[0] += t[0];
-    s[1] += t[1];
-    s[2] += t[2];
-    s[3] += t[3];
+  f32x4 t[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) t[k] = *reinterpret_cast<const f32x4*>(src + k * slab);
+  f32x4 s = t[0];
+#pragma unroll
+  for (int k = 1; k < NS; ++k) {
+    s[0] += t[k][0];
+    s[1] += t[k][1];
+    s[2] += t[k][2];
+    s[3] += t[k][3];
   }
   float v[4] = {s[0], s[1], s[2], s[3]};
   epilogue_group<bf16>(p, m, n, v);
+}
+
+void splitk_reduce(const GemmParams& p, int nsplit, hipStream_t s) {
+  const long long nq = (long long)p.M * (p.n_store / 4);
+  const dim3 grid(static_cast<unsigned>((nq + 255) / 256));
+  switch (nsplit) {
+    case 2: hipLaunchKernelGGL(splitk_reduce_kernel<2>, grid, dim3(256), 0, s, p); break;
+    case 3: hipLaunchKernelGGL(splitk_reduce_kernel<3>, grid, dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL(splitk_reduce_kernel<4>, grid, dim3(256), 0, s, p); break;
+    case 5: hipLaunchKernelGGL(splitk_reduce_kernel<5>, grid, dim3(256), 0, s, p); break;
+    case 6: hipLaunchKernelGGL(splitk_reduce_kernel<6>, grid, dim3(256), 0, s, p); break;
+    case 7: hipLaunchKernelGGL(splitk_reduce_kernel<7>, grid, dim3(256), 0, s, p); break;
+    case 8: hipLaunchKernelGGL(splitk_reduce_kernel<8>, grid, dim3(256), 0, s, p); break;
+    default: throw Error(-1, "gemm: split-K reduction takes 2 to 8 slabs");
+  }
+  DN_HIP(hipGetLastError());
 }
 
 template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE>
@@ -620,10 +639,7 @@ void run_frag(const GemmParams& p, int nsplit, hipStream_t s) {
     launch_frag<BM, FN, S, D, WPE, MODE, true, PRE>(p, nsplit, s);
   } else if (nsplit > 1) {
     launch_frag<BM, FN, S, D, WPE, MODE, true, PRE>(p, nsplit, s);
-    const long long nq = (long long)p.M * (p.n_store / 4);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, p,
-                       nsplit);
-    DN_HIP(hipGetLastError());
+    splitk_reduce(p, nsplit, s);
   } else {
     launch_frag<BM, FN, S, D, WPE, MODE, false, PRE>(p, 1, s);
   }

@@ -68,14 +68,25 @@ __global__ __launch_bounds__(256) void gn_partial_kernel(GroupNormParams p, GnGe
       ld = p.c1;
       c -= p.c0;
     }
+    // all of the thread's pixels are loaded first (clamped to the image), then summed
+    // in pixel order
     const int pbeg = chunk * g.pix_per_chunk;
     const int pend = min(pbeg + g.pix_per_chunk, p.HW);
-    for (int px = pbeg + pl; px < pend; px += pl_count) {
-      const uint4 raw = ld16(src + ((long long)n * p.HW + px) * ld + c);
-      const T* xv = reinterpret_cast<const T*>(&raw);
+    uint4 raw[kPixPerThread];
+#pragma unroll
+    for (int t = 0; t < kPixPerThread; ++t) {
+      const int px = min(pbeg + pl + t * pl_count, p.HW - 1);
+      raw[t] = ld16(src + ((long long)n * p.HW + px) * ld + c);
+    }
+#pragma unroll
+    for (int t = 0; t < kPixPerThread; ++t) {
+      // pixels past the chunk add an exact zero (a select, so that no branch sinks the
+      // loads back to their uses)
+      const bool in = pbeg + pl + t * pl_count < pend;
+      const T* xv = reinterpret_cast<const T*>(&raw[t]);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float x = to_f32(xv[e]);
+        const float x = in ? to_f32(xv[e]) : 0.f;
         s[e] += x;
         q[e] += x * x;
       }
@@ -167,37 +178,57 @@ __global__ __launch_bounds__(256) void gn_apply_kernel(GroupNormParams p, GnGeom
   const float* scale = p.stats + (long long)n * g.C;
   const float* shift = p.stats + (long long)(p.n + n) * g.C;
   const long long rowbase = (long long)n * p.HW + pix0;
-  for (; q < npix;) {
-    const long long pix = rowbase + q;
-    const int c = r * VEC;
-    const uint4 raw = c < p.c0 ? ld16(static_cast<const T*>(p.x0) + pix * p.c0 + c)
-                               : ld16(static_cast<const T*>(p.x1) + pix * p.c1 + (c - p.c0));
-    const T* xv = reinterpret_cast<const T*>(&raw);
-    uint4 outv;
-    T* ov = reinterpret_cast<T*>(&outv);
+  // the block's (pixel, vector) pairs, 256 at a time, in batches of kBatch per thread
+  // whose loads are all issued before the batch is computed and stored
+  constexpr int kBatch = 4;
+  const int nit = (npix * V + 255) / 256;  // pairs per thread, rounded up
+  for (int b0 = 0; b0 < nit; b0 += kBatch) {
+    uint4 raw[kBatch];
+    float4 sc[kBatch][VEC / 4], sh[kBatch][VEC / 4];
+    int qq[kBatch], cc[kBatch];
 #pragma unroll
-    for (int e = 0; e < VEC; e += 4) {
-      const float4 sc = *reinterpret_cast<const float4*>(scale + c + e);
-      const float4 sh = *reinterpret_cast<const float4*>(shift + c + e);
-      float v0 = to_f32(xv[e + 0]) * sc.x + sh.x, v1 = to_f32(xv[e + 1]) * sc.y + sh.y;
-      float v2 = to_f32(xv[e + 2]) * sc.z + sh.z, v3 = to_f32(xv[e + 3]) * sc.w + sh.w;
-      if (p.silu) {
-        v0 = silu_f(v0);
-        v1 = silu_f(v1);
-        v2 = silu_f(v2);
-        v3 = silu_f(v3);
+    for (int u = 0; u < kBatch; ++u) {
+      qq[u] = q;
+      cc[u] = r * VEC;
+      const long long pix = rowbase + min(q, npix - 1);
+      const int c = r * VEC;
+      raw[u] = c < p.c0 ? ld16(static_cast<const T*>(p.x0) + pix * p.c0 + c)
+                        : ld16(static_cast<const T*>(p.x1) + pix * p.c1 + (c - p.c0));
+#pragma unroll
+      for (int e = 0; e < VEC / 4; ++e) {
+        sc[u][e] = *reinterpret_cast<const float4*>(scale + c + 4 * e);
+        sh[u][e] = *reinterpret_cast<const float4*>(shift + c + 4 * e);
       }
-      ov[e + 0] = from_f32<T>(v0);
-      ov[e + 1] = from_f32<T>(v1);
-      ov[e + 2] = from_f32<T>(v2);
-      ov[e + 3] = from_f32<T>(v3);
+      q += step_q;
+      r += step_r;
+      if (r >= V) {
+        r -= V;
+        ++q;
+      }
     }
-    st16(static_cast<T*>(p.y) + pix * g.C + c, outv);
-    q += step_q;
-    r += step_r;
-    if (r >= V) {
-      r -= V;
-      ++q;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (qq[u] >= npix) continue;
+      const T* xv = reinterpret_cast<const T*>(&raw[u]);
+      uint4 outv;
+      T* ov = reinterpret_cast<T*>(&outv);
+#pragma unroll
+      for (int e = 0; e < VEC; e += 4) {
+        const float4 a = sc[u][e / 4], bsh = sh[u][e / 4];
+        float v0 = to_f32(xv[e + 0]) * a.x + bsh.x, v1 = to_f32(xv[e + 1]) * a.y + bsh.y;
+        float v2 = to_f32(xv[e + 2]) * a.z + bsh.z, v3 = to_f32(xv[e + 3]) * a.w + bsh.w;
+        if (p.silu) {
+          v0 = silu_f(v0);
+          v1 = silu_f(v1);
+          v2 = silu_f(v2);
+          v3 = silu_f(v3);
+        }
+        ov[e + 0] = from_f32<T>(v0);
+        ov[e + 1] = from_f32<T>(v1);
+        ov[e + 2] = from_f32<T>(v2);
+        ov[e + 3] = from_f32<T>(v3);
+      }
+      st16(static_cast<T*>(p.y) + (rowbase + qq[u]) * g.C + cc[u], outv);
     }
   }
 }
