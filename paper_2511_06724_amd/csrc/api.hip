@@ -77,7 +77,7 @@ template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
       DN_HIP(hipMemset(d.zero, 0, 256));
       d.cus = prop.multiProcessorCount;
     }
-    const dn::GemmPlan g0 = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, d.cus, p.vt == nullptr);
+    const dn::GemmPlan g0 = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, d.cus, p.vt == nullptr, false, p.taps == 9);
     const size_t need = dn::gemm_workspace_floats(g0, p.M, p.N);
     if (need > d.part_floats) {
       if (d.part) {
@@ -91,7 +91,7 @@ template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
     }
     w = d;
   }
-  const dn::GemmPlan g = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, w.cus, p.vt == nullptr);
+  const dn::GemmPlan g = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, w.cus, p.vt == nullptr, false, p.taps == 9);
   p.zero16 = w.zero;
   p.part = w.part;
   p.part_floats = w.part_floats;

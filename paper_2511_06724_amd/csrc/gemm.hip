@@ -267,23 +267,29 @@ template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPl
 // Fragment-B kernel (bf16 weights in fragment order). Three tile variants share a CU
 // between several workgroups: 128 x 256 (two per CU), 128 x 128 (two) and 64 x 128
 // (four). The plan minimises a cost model fitted to measured SD-XL GEMM times on MI355X
-// (bf16, weights streamed from HBM): a run takes ceil(units / slots) rounds, a round
+// (bf16, weights streamed from HBM; one fit for the linear layers, one for the implicit
+// convolutions): a run takes ceil(units / slots) rounds, a round
 // costs the MFMA work of the units resident on a CU at a per-CU rate R plus a fixed
 // prologue cost O; the epilogue adds E per million outputs, and a K split adds the fp32
 // slabs written and read by the reduction (only the extra slab reads when the consumer
 // sums the slabs itself). GEGLU needs 64-column value/gate pairs per wave (128 x 256).
-GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce) {
+GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce, bool conv) {
   struct Var {
     int bm, bn, wg;
     double rate, fixed, epi;  // FLOP per us per CU, us per round, us per 1e6 outputs
   };
-  static const Var vars[] = {{128, 256, 2, 2.4e6, 1.0, 2.0}, {128, 128, 2, 1.6e6, 3.0, 0.0}, {64, 128, 4, 1.6e6, 1.0, 0.0}};
+  // separate fits for the linear layers and the implicit convolutions (whose A gather
+  // and tap masks change the per-stage cost)
+  static const Var lin_vars[] = {{128, 256, 2, 2.4e6, 5.0, 1.0}, {128, 128, 2, 2.0e6, 8.0, 0.0}, {64, 128, 4, 1.6e6, 3.0, 0.0}};
+  static const Var conv_vars[] = {{128, 256, 2, 2.4e6, 1.0, 2.0}, {128, 128, 2, 1.6e6, 3.0, 0.0}, {64, 128, 4, 1.6e6, 1.0, 0.0}};
+  const Var* vars = conv ? conv_vars : lin_vars;
   GemmPlan best{128, 256, 0};
   best.stages = 3;
   best.frag = 1;
   double best_t = 1e300;
   const int nk = K / 64;
-  for (const Var& v : vars) {
+  for (int vi = 0; vi < 3; ++vi) {
+    const Var& v = vars[vi];
     if (geglu && v.bn != 256) continue;
     const long long tiles = (long long)ceil_div(M, v.bm) * ceil_div(N, v.bn);
     for (int sp = 1; sp <= kMaxSplit; ++sp) {
@@ -306,8 +312,8 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
 }
 
 template <typename T>
-GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce) {
-  if (sizeof(T) == 2 && gemm_frag_layout(N, K)) return frag_plan(M, N, K, geglu, cus, allow_split, fused_reduce);
+GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce, bool conv) {
+  if (sizeof(T) == 2 && gemm_frag_layout(N, K)) return frag_plan(M, N, K, geglu, cus, allow_split, fused_reduce, conv);
   const long long t128 = (long long)ceil_div(M, 128) * ceil_div(N, 128);
   if (sizeof(T) == 2 && N >= 128 && K % 64 == 0 && M >= 8192) {
     const long long t256 = (long long)ceil_div(M, 256) * ceil_div(N, 256);
@@ -349,8 +355,8 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
     dispatch<T, false>(p, g, s);
 }
 
-template GemmPlan gemm_plan<float>(int, int, int, int, int, bool, bool);
-template GemmPlan gemm_plan<bf16>(int, int, int, int, int, bool, bool);
+template GemmPlan gemm_plan<float>(int, int, int, int, int, bool, bool, bool);
+template GemmPlan gemm_plan<bf16>(int, int, int, int, int, bool, bool, bool);
 template void gemm<float>(const GemmParams&, const GemmPlan&, hipStream_t);
 template void gemm<bf16>(const GemmParams&, const GemmPlan&, hipStream_t);
 

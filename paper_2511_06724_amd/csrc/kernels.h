@@ -65,7 +65,8 @@ constexpr int kMaxSplit = 8;
 // fused_reduce: the partial slabs are summed by the consumer (layernorm_reduce), so a
 // split costs only the extra slab reads.
 template <typename T>
-GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split = true, bool fused_reduce = false);
+GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split = true, bool fused_reduce = false,
+                   bool conv = false);
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 void gemm_bf16_dma(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s);

@@ -773,7 +773,7 @@ template <typename T> struct Exec {
   size_t split_need = 0;  // dry walk: largest split-K workspace (floats) of the step
 
   void run_gemm(GemmParams& p) {
-    const GemmPlan g = gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus, p.vt == nullptr);
+    const GemmPlan g = gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus, p.vt == nullptr, false, p.taps == 9);
     if (dry) {
       split_need = std::max(split_need, gemm_workspace_floats(g, p.M, p.N));
       return;
