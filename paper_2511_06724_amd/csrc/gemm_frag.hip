@@ -341,17 +341,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
       KSched<0, 4 * NM, 4 * FM, 4 * FN>::apply();
       __builtin_amdgcn_sched_barrier(0);
     };
-    if constexpr (D == 2) {
-      for (int kt = kt0; kt < kt1; kt += 2) {
-        pstage(kt, sa[0], sa[1], bq[0]);
-        if (kt + 1 < kt1) pstage(kt + 1, sa[1], sa[0], bq[D - 1]);
-      }
-    } else {
-      for (int kt = kt0; kt < kt1; kt += 2) {
-        pstage(kt, sa[0], sa[1], bq[0]);
-        if (kt + 1 < kt1) pstage(kt + 1, sa[1], sa[0], bq[0]);
-      }
+    // Pairs of stages, then the odd one: no stage of the loop body is conditional, so the
+    // compiler's wait for a B register counts both stages' loads issued after it.
+    int kt = kt0;
+    for (; kt + 1 < kt1; kt += 2) {
+      pstage(kt, sa[0], sa[1], bq[0]);
+      pstage(kt + 1, sa[1], sa[0], bq[D - 1]);
     }
+    if (kt < kt1) pstage(kt, sa[0], sa[1], bq[0]);
   } else {
     BReg bq[D];
     // One k-step: [the DMA of a later A stage first, when `dma`], the next k-step's A
@@ -406,10 +403,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
     };
 
     if constexpr (D == 2) {
-      for (int kt = kt0; kt < kt1; kt += 2) {
+      // Pairs of stages, then the odd one: no stage of the loop body is conditional, so
+      // the compiler's wait for a B register counts both stages' loads issued after it.
+      int kt = kt0;
+      for (; kt + 1 < kt1; kt += 2) {
         stage(kt, bq[0]);
-        if (kt + 1 < kt1) stage(kt + 1, bq[D - 1]);
+        stage(kt + 1, bq[1]);
       }
+      if (kt < kt1) stage(kt, bq[0]);
     } else {
       for (int kt = kt0; kt < kt1; ++kt) stage(kt, bq[0]);
     }
