@@ -271,8 +271,9 @@ template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPl
 // convolutions): a run takes ceil(units / slots) rounds, a round
 // costs the MFMA work of the units resident on a CU at a per-CU rate R plus a fixed
 // prologue cost O; the epilogue adds E per million outputs, and a K split adds the fp32
-// slabs written and read by the reduction (only the extra slab reads when the consumer
-// sums the slabs itself). GEGLU needs 64-column value/gate pairs per wave (128 x 256).
+// slabs written and read by the reduction (when the consumer, a LayerNorm, sums the
+// slabs itself: its extra slab reads, at the cost per slab measured for that kernel
+// together with the GEMM). GEGLU needs 64-column value/gate pairs per wave (128 x 256).
 GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce, bool conv) {
   struct Var {
     int bm, bn, wg;
@@ -299,7 +300,7 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
       const long long rounds = (units + slots - 1) / slots;
       const double per_cu = std::max(1.0, (double)std::min(units, slots) / cus);
       double t = rounds * (per_cu * 2.0 * v.bm * v.bn * ((double)K / sp) / v.rate + v.fixed) + v.epi * M * N / 1e6;
-      if (sp > 1) t += fused_reduce ? 0.1 * (sp - 1.0) * M * N * 4.0 / 1e6 : 0.1 * (sp + 1.0) * M * N * 4.0 / 1e6 + 2.0;
+      if (sp > 1) t += fused_reduce ? 0.3 * (sp - 1.0) * M * N * 4.0 / 1e6 : 0.1 * (sp + 1.0) * M * N * 4.0 / 1e6 + 2.0;
       if (t < best_t) {
         best_t = t;
         best.bm = v.bm;
