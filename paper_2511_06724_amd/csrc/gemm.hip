@@ -19,6 +19,7 @@
 // workgroup ids go round-robin over the 8 XCDs) works through a contiguous band
 // of output columns with all row tiles, keeping that band of B in its L2.
 #include <algorithm>
+#include <cmath>
 
 #include "gemm_epilogue.h"
 
@@ -282,8 +283,11 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
   // separate fits for the linear layers and the implicit convolutions (whose A gather
   // and tap masks change the per-stage cost)
   static const Var lin_vars[] = {{128, 256, 2, 2.4e6, 5.0, 1.0}, {128, 128, 2, 2.0e6, 8.0, 0.0}, {64, 128, 4, 1.6e6, 3.0, 0.0}};
-  static const Var conv_vars[] = {{128, 256, 2, 2.4e6, 1.0, 2.0}, {128, 128, 2, 1.6e6, 3.0, 0.0}, {64, 128, 4, 1.6e6, 1.0, 0.0}};
+  static const Var conv_vars[] = {{128, 256, 2, 2.4e6, 5.0, 3.0}, {128, 128, 2, 1.6e6, 1.0, 0.0}, {64, 128, 4, 1.6e6, 1.0, 0.0}};
   const Var* vars = conv ? conv_vars : lin_vars;
+  // convolutions: a partly filled round costs more than its average load per CU (the
+  // CUs that hold one more unit finish last)
+  const double fill_penalty = conv ? 0.25 : 0.0;
   GemmPlan best{128, 256, 0};
   best.stages = 3;
   best.frag = 1;
@@ -298,7 +302,8 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
       const long long units = tiles * sp;
       const long long slots = (long long)cus * v.wg;
       const long long rounds = (units + slots - 1) / slots;
-      const double per_cu = std::max(1.0, (double)std::min(units, slots) / cus);
+      const double load = (double)std::min(units, slots) / cus;
+      const double per_cu = std::max(1.0, load) + fill_penalty * (std::ceil(load) - load);
       double t = rounds * (per_cu * 2.0 * v.bm * v.bn * ((double)K / sp) / v.rate + v.fixed) + v.epi * M * N / 1e6;
       if (sp > 1) t += fused_reduce ? 0.3 * (sp - 1.0) * M * N * 4.0 / 1e6 : 0.1 * (sp + 1.0) * M * N * 4.0 / 1e6 + 2.0;
       if (t < best_t) {
