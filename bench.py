@@ -162,17 +162,13 @@ def profile_kernel(torch, dn):
                       "kernel_source_hash": kernel_source_hash()}))
 
 
-def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, queries=4):
-    """Approximate caching: lookup + latent fetch + resume at k for 50 - k steps."""
+def lookup_timing(torch, dn, n_entries=100_000, dim=768, queries=4):
+    """Nearest-prompt lookup over n_entries cached fp16 embeddings: host time of the
+    synchronous call with the table resident in the last-level cache (warm) and after
+    it was evicted (cold). Returns (cache, device queries, planted rows, figures)."""
     from paper_2511_06724_amd import workloads as W
     cache = torch.from_numpy(W.cache_embeddings(n_entries, dim, seed=7).view("uint16")).cuda()
     qs, rows = W.planted_queries(cache.cpu().numpy().view("float16"), queries, seed=9)
-    # cached latents: 100,000 x 4 x 128 x 128 bf16 = 13.1 GB, drawn on the device
-    g = torch.Generator(device="cuda").manual_seed(8)
-    lat_cache = torch.empty((n_entries, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda",
-                            dtype=torch.bfloat16)
-    for s in range(0, n_entries, 10_000):
-        lat_cache[s:s + 10_000].normal_(generator=g)
     qd = [torch.from_numpy(q.view("uint16").copy()).cuda() for q in qs]
     # warm: the 153.6 MB table stays in the 256 MB last-level cache between queries
     dn.ac_lookup(qd[0], cache)
@@ -182,25 +178,41 @@ def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, queries
         for q in qd:
             dn.ac_lookup(q, cache)
     t_warm = (time.perf_counter() - t0) / (4 * len(qd))
-    # cold: a 1 GiB write between queries evicts the table from the last-level cache
-    flush = torch.empty(256 << 20, device="cuda", dtype=torch.float32)
+    # cold: reading 1 GiB between queries evicts the table from the 256 MB last-level
+    # cache with clean lines (a write would leave dirty lines whose write-back then
+    # competes with the scan)
+    flush = torch.zeros(256 << 20, device="cuda", dtype=torch.float32)
     t_cold = 0.0
     for q in qd:
-        flush.fill_(0.0)
+        flush.sum()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         dn.ac_lookup(q, cache)
         t_cold += time.perf_counter() - t0
     t_cold /= len(qd)
     del flush
-    t_lookup = t_warm
     ok = all(dn.ac_lookup(q, cache)[0] == int(r) for q, r in zip(qd, rows))
-    lat = torch.empty((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda")
-    out = {"lookup_us_per_query_warm": round(t_warm * 1e6, 1), "lookup_us_per_query_cold": round(t_cold * 1e6, 1),
+    fig = {"lookup_us_per_query_warm": round(t_warm * 1e6, 1), "lookup_us_per_query_cold": round(t_cold * 1e6, 1),
            "lookup_GBps_warm": round(n_entries * dim * 2 / t_warm / 1e9, 1),
            "lookup_GBps_cold": round(n_entries * dim * 2 / t_cold / 1e9, 1),
-           "lookup_note": "synchronous call timed on the host (includes launch and the 16-byte result copy)",
-           "planted_found": ok, "queries_per_k": 2, "images_per_s_by_k": {}}
+           "lookup_note": "synchronous call timed on the host (includes the two launches and the 12-byte "
+                          "result copy); the kernels alone: profiles/ac_lookup_kernels.md",
+           "planted_found": ok}
+    return cache, qd, rows, fig
+
+
+def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, queries=4):
+    """Approximate caching: lookup + latent fetch + resume at k for 50 - k steps."""
+    cache, qd, rows, fig = lookup_timing(torch, dn, n_entries, dim, queries)
+    # cached latents: 100,000 x 4 x 128 x 128 bf16 = 13.1 GB, drawn on the device
+    g = torch.Generator(device="cuda").manual_seed(8)
+    lat_cache = torch.empty((n_entries, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda",
+                            dtype=torch.bfloat16)
+    for s in range(0, n_entries, 10_000):
+        lat_cache[s:s + 10_000].normal_(generator=g)
+    lat = torch.empty((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda")
+    out = dict(fig)
+    out.update({"queries_per_k": 2, "images_per_s_by_k": {}})
     for k in (0, 5, 10, 15, 20, 25):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -315,6 +327,8 @@ def main():
     ap.add_argument("--no-ac", action="store_true")
     ap.add_argument("--profile-kernel", action="store_true",
                     help="only launch the FF-in GEMM 20 times and a 256 MiB copy (counter collection)")
+    ap.add_argument("--lookup-only", action="store_true",
+                    help="only the cache lookup (100,000 x 768 fp16, warm and cold): one JSON line")
     ap.add_argument("--sweep-batch", action="store_true",
                     help="instead of the headline line: latency and images/s for batch 1, 2, 4, 8 and the "
                          "smaller variant (4 / 1 transformer blocks per 32x32 / 64x64 stage)")
@@ -334,6 +348,9 @@ def main():
         return
     if args.sweep_batch:
         sweep_batch(torch, dn, W, args)
+        return
+    if args.lookup_only:
+        print(json.dumps(lookup_timing(torch, dn)[3]))
         return
     cfg = W.sdxl(W.DN_BF16, batch=args.batch)
     print("[bench] generating SD-XL weights on the device", file=sys.stderr, flush=True)

@@ -188,7 +188,11 @@ dn_status dn_unet_eps(dn_handle* h, const float* x, int32_t t, const float* text
  * (row-major). Products and sums in fp32. On success *out_idx (host) receives
  * the index and, if out_score (host) is not NULL, *out_score the cosine.
  * Synchronous (default stream). n >= 1, dim >= 1; the query must be non-zero.
- * On error *out_idx is left untouched (the caller falls back to K = 0). */
+ * On error *out_idx is left untouched (the caller falls back to K = 0).
+ * The first call on a device allocates that device's scan workspace (32 KB) and a
+ * 256-byte pinned host buffer the result is written to; both are kept until the
+ * process ends, and calls that overlap on one device (from several threads) race
+ * on them. */
 dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64_t n, int32_t dim,
                     int64_t* out_idx, float* out_score);
 

@@ -35,18 +35,30 @@ template <typename F> dn_status guarded(F&& f) {
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
-// Per-device workspace of the cache lookup (partials + result), grown once.
+// Per-device state of the cache lookup, allocated once: the device workspace of the
+// per-workgroup winners, and a pinned host buffer the reduction writes the result to
+// (index at byte 0, score at byte 8), so no copy follows the kernels.
+struct LookupRes {
+  long long idx;
+  float score;
+};
 struct LookupWs {
   std::mutex mu;
   std::vector<void*> ws;
+  std::vector<LookupRes*> res;
 };
 LookupWs g_lookup;
 
-void* lookup_ws(int dev) {
+void lookup_state(int dev, void** ws, LookupRes** res) {
   std::lock_guard<std::mutex> lk(g_lookup.mu);
-  if ((int)g_lookup.ws.size() <= dev) g_lookup.ws.resize(dev + 1, nullptr);
-  if (!g_lookup.ws[dev]) DN_HIP(hipMalloc(&g_lookup.ws[dev], dn::lookup_workspace_bytes() + 256));
-  return g_lookup.ws[dev];
+  if ((int)g_lookup.ws.size() <= dev) {
+    g_lookup.ws.resize(dev + 1, nullptr);
+    g_lookup.res.resize(dev + 1, nullptr);
+  }
+  if (!g_lookup.ws[dev]) DN_HIP(hipMalloc(&g_lookup.ws[dev], dn::lookup_workspace_bytes()));
+  if (!g_lookup.res[dev]) DN_HIP(hipHostMalloc(reinterpret_cast<void**>(&g_lookup.res[dev]), 256));
+  *ws = g_lookup.ws[dev];
+  *res = g_lookup.res[dev];
 }
 
 bool is_dtype(int32_t d) { return d == DN_FP32 || d == DN_BF16; }
@@ -170,14 +182,16 @@ dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64
     DN_CHECK(dim >= 1, "ac_lookup: dim must be >= 1");
     int dev = 0;
     DN_HIP(hipGetDevice(&dev));
-    char* ws = static_cast<char*>(lookup_ws(dev));
-    long long* idx_dev = reinterpret_cast<long long*>(ws + dn::lookup_workspace_bytes());
-    float* score_dev = reinterpret_cast<float*>(ws + dn::lookup_workspace_bytes() + 8);
-    dn::lookup(query_emb, cache_embs, n, dim, ws, idx_dev, score_dev, nullptr);
-    long long idx = -1;
-    float score = 0.f;
-    DN_HIP(hipMemcpy(&idx, idx_dev, sizeof(idx), hipMemcpyDeviceToHost));
-    DN_HIP(hipMemcpy(&score, score_dev, sizeof(score), hipMemcpyDeviceToHost));
+    void* ws = nullptr;
+    LookupRes* res = nullptr;
+    lookup_state(dev, &ws, &res);
+    res->idx = -1;
+    res->score = 0.f;
+    dn::lookup(query_emb, cache_embs, n, dim, ws, &res->idx, &res->score, nullptr);
+    DN_HIP(hipStreamSynchronize(nullptr));
+    // written by the device: read through volatile so the values set above are not reused
+    const long long idx = *static_cast<volatile long long*>(&res->idx);
+    const float score = *static_cast<volatile float*>(&res->score);
     DN_CHECK(idx >= 0 && idx < n, "ac_lookup: no row scored (zero query or zero-norm cache)");
     *out_idx = idx;
     if (out_score) *out_score = score;

@@ -164,8 +164,11 @@ template <typename T> void pack(const PackParams& p, hipStream_t s);
 void pack_bias(float* dst, int n, const float* src, int src_n, int row_mode, int D, int Dp, hipStream_t s);
 
 // ---------------------------------------------------------------- cache lookup
+// Top-1 cosine row of cache [n][dim] (fp16) for q [dim]: writes the index (-1 when no
+// row has a defined cosine) and the cosine to idx_out / score_out, which may be device
+// memory or pinned host memory. ws: lookup_workspace_bytes() of device memory.
 size_t lookup_workspace_bytes();
-void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_dev,
-            float* score_dev, hipStream_t s);
+void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_out,
+            float* score_out, hipStream_t s);
 
 }  // namespace dn

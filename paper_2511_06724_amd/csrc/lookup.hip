@@ -1,17 +1,18 @@
 // Top-1 cosine search over the prompt-embedding cache (HBM-bound; gfx950).
 //
-// Pass 1: every half-wave (32 lanes) scores one cache row at a time — 16-byte
-// coalesced fp16 loads, fp32 products and sums of q.c and c.c, a 5-step
-// butterfly — and keeps its best (score, index); each workgroup writes the
-// best of its 8 half-waves. Pass 2: one workgroup reduces the per-workgroup
-// winners. Ties go to the lowest index at every stage, so the result is the
-// first maximum, independent of the launch shape.
+// Pass 1: every half-wave (32 lanes) scores two cache rows per iteration — all
+// 16-byte coalesced fp16 loads of both rows issued before any arithmetic, packed
+// fp16 dot products accumulating in fp32 (v_dot2_f32_f16: the fp16 x fp16 products
+// are exact in fp32) for q.c and c.c, then 5-step butterflies — and keeps its best
+// (score, index); each workgroup writes the best of its 8 half-waves. Pass 2: one
+// workgroup reduces the per-workgroup winners. Ties go to the lowest index at every
+// stage, so the result is the first maximum, independent of the launch shape.
 #include "kernels.h"
 
 namespace dn {
 namespace {
 
-constexpr int kScanBlocks = 2048;
+constexpr int kScanBlocks = 2048;  // a multiple of 256 (the reduction's per-thread share)
 constexpr int kQMaxVec = 4;  // fast path: dim <= 32 lanes * 4 vectors * 8 = 1024
 
 struct Cand {
@@ -34,6 +35,21 @@ __device__ __forceinline__ float half_sum(float v) {
 // Score of one row (cosine up to the positive factor 1/|q|); -inf for a zero row.
 __device__ __forceinline__ float row_score(float dot, float cc) { return cc > 0.f ? dot * rsqrtf(cc) : -INFINITY; }
 
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ h2 as_h2(unsigned u) { return __builtin_bit_cast(h2, u); }
+
+// q . x and x . x over one 16-byte vector (8 fp16 values), accumulated in fp32.
+__device__ __forceinline__ void dot8(const h2 (&qv)[4], const uint4 x, float& dot, float& cc) {
+  const unsigned w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const h2 v = as_h2(w[k]);
+    dot = __builtin_amdgcn_fdot2(qv[k], v, dot, false);
+    cc = __builtin_amdgcn_fdot2(v, v, cc, false);
+  }
+}
+
 template <int NQ>
 __global__ __launch_bounds__(256) void scan_vec_kernel(const uint16_t* q, const uint16_t* cache, long long n, int dim,
                                                        Cand* part) {
@@ -41,41 +57,56 @@ __global__ __launch_bounds__(256) void scan_vec_kernel(const uint16_t* q, const 
   const int li = lane & 31;
   const int hw = threadIdx.x >> 5;  // half-wave in block, 0..7
   const int V = dim / 8;
-  float qv[NQ][8];
+  h2 qv[NQ][4];
+  bool act[NQ];
 #pragma unroll
   for (int j = 0; j < NQ; ++j) {
     const int v = li + 32 * j;
-    uint4 raw = v < V ? ld16(q + v * 8) : make_uint4(0u, 0u, 0u, 0u);
-    const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) qv[j][e] = h2f(h[e]);
+    act[j] = v < V;
+    const uint4 raw = act[j] ? ld16(q + v * 8) : make_uint4(0u, 0u, 0u, 0u);
+    qv[j][0] = as_h2(raw.x);
+    qv[j][1] = as_h2(raw.y);
+    qv[j][2] = as_h2(raw.z);
+    qv[j][3] = as_h2(raw.w);
   }
   float best_s = -INFINITY;
   long long best_i = n;
-  const long long stride = (long long)gridDim.x * 8;
-  for (long long row = (long long)blockIdx.x * 8 + hw; row < n; row += stride) {
-    const uint16_t* c = cache + row * dim;
-    float dot = 0.f, cc = 0.f;
+  const long long stride = (long long)gridDim.x * 16;
+  // rows r and r + 1 per half-wave; past the end the second row re-reads row r and is not scored
+  for (long long r = (long long)blockIdx.x * 16 + 2 * hw; r < n; r += stride) {
+    const bool two = r + 1 < n;
+    const uint16_t* c0 = cache + r * dim;
+    const uint16_t* c1 = two ? c0 + dim : c0;
+    uint4 x0[NQ], x1[NQ];
 #pragma unroll
     for (int j = 0; j < NQ; ++j) {
-      const int v = li + 32 * j;
-      if (v < V) {
-        const uint4 raw = ld16(c + v * 8);
-        const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float x = h2f(h[e]);
-          dot += qv[j][e] * x;
-          cc += x * x;
-        }
-      }
+      const int v = act[j] ? li + 32 * j : 0;
+      x0[j] = ld16(c0 + v * 8);
+      x1[j] = ld16(c1 + v * 8);
     }
-    dot = half_sum(dot);
-    cc = half_sum(cc);
-    const float s = row_score(dot, cc);
-    if (better(s, row, best_s, best_i)) {
-      best_s = s;
-      best_i = row;
+    float d0 = 0.f, s0 = 0.f, d1 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+      if (!act[j]) continue;
+      dot8(qv[j], x0[j], d0, s0);
+      dot8(qv[j], x1[j], d1, s1);
+    }
+#pragma unroll
+    for (int o = 16; o > 0; o >>= 1) {
+      d0 += __shfl_xor(d0, o, 64);
+      s0 += __shfl_xor(s0, o, 64);
+      d1 += __shfl_xor(d1, o, 64);
+      s1 += __shfl_xor(s1, o, 64);
+    }
+    const float sc0 = row_score(d0, s0);
+    if (better(sc0, r, best_s, best_i)) {
+      best_s = sc0;
+      best_i = r;
+    }
+    const float sc1 = row_score(d1, s1);
+    if (two && better(sc1, r + 1, best_s, best_i)) {
+      best_s = sc1;
+      best_i = r + 1;
     }
   }
   __shared__ Cand red[8];
@@ -127,42 +158,63 @@ __global__ __launch_bounds__(256) void scan_scalar_kernel(const uint16_t* q, con
   }
 }
 
+// Pass 2, one workgroup: every thread loads its (up to kScanBlocks / 256) winners
+// before comparing them; waves reduce with shuffles, then the 4 wave winners in order.
+// The squared norm of q (for the reported cosine) is summed alongside. The result may
+// be written to pinned host memory.
 __global__ __launch_bounds__(256) void reduce_kernel(const Cand* part, int nb, const uint16_t* q, int dim,
                                                      long long* idx, float* score) {
-  __shared__ float ss[256];
-  __shared__ long long si[256];
-  __shared__ float qn[256];
-  const int t = threadIdx.x;
-  float bs = -INFINITY;
-  long long bi = 0x7fffffffffffffffll;
-  for (int k = t; k < nb; k += 256)
-    if (better(part[k].s, part[k].i, bs, bi)) {
-      bs = part[k].s;
-      bi = part[k].i;
-    }
+  constexpr int kPer = kScanBlocks / 256;
+  __shared__ float ws_s[4], ws_q[4];
+  __shared__ long long ws_i[4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  Cand c[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int j = t + 256 * k;
+    c[k] = j < nb ? part[j] : Cand{-INFINITY, 0x7fffffffffffffffll};
+  }
   float qq = 0.f;
   for (int e = t; e < dim; e += 256) {
     const float x = h2f(q[e]);
     qq += x * x;
   }
-  ss[t] = bs;
-  si[t] = bi;
-  qn[t] = qq;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (t < w) {
-      if (better(ss[t + w], si[t + w], ss[t], si[t])) {
-        ss[t] = ss[t + w];
-        si[t] = si[t + w];
-      }
-      qn[t] += qn[t + w];
+  float bs = c[0].s;
+  long long bi = c[0].i;
+#pragma unroll
+  for (int k = 1; k < kPer; ++k)
+    if (better(c[k].s, c[k].i, bs, bi)) {
+      bs = c[k].s;
+      bi = c[k].i;
     }
-    __syncthreads();
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float s2 = __shfl_xor(bs, o, 64);
+    const long long i2 = __shfl_xor(bi, o, 64);
+    if (better(s2, i2, bs, bi)) {
+      bs = s2;
+      bi = i2;
+    }
+    qq += __shfl_xor(qq, o, 64);
   }
+  if (lane == 0) {
+    ws_s[w] = bs;
+    ws_i[w] = bi;
+    ws_q[w] = qq;
+  }
+  __syncthreads();
   if (t == 0) {
+    float qn = ws_q[0];
+    for (int k = 1; k < 4; ++k) {
+      if (better(ws_s[k], ws_i[k], bs, bi)) {
+        bs = ws_s[k];
+        bi = ws_i[k];
+      }
+      qn += ws_q[k];
+    }
     // A zero query (or a cache of zero rows) has no defined cosine: report no row.
-    *idx = (qn[0] > 0.f && ss[0] > -INFINITY) ? si[0] : -1;
-    *score = ss[0] * rsqrtf(qn[0]);
+    *idx = (qn > 0.f && bs > -INFINITY) ? bi : -1;
+    *score = bs * rsqrtf(qn);
   }
 }
 
@@ -170,11 +222,11 @@ __global__ __launch_bounds__(256) void reduce_kernel(const Cand* part, int nb, c
 
 size_t lookup_workspace_bytes() { return sizeof(Cand) * kScanBlocks; }
 
-void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_dev,
-            float* score_dev, hipStream_t s) {
+void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_out,
+            float* score_out, hipStream_t s) {
   DN_CHECK(n >= 1 && dim >= 1, "lookup: empty cache");
   Cand* part = static_cast<Cand*>(ws);
-  const long long want = (n + 7) / 8;
+  const long long want = (n + 15) / 16;
   const int nb = static_cast<int>(want < kScanBlocks ? want : kScanBlocks);
   const bool aligned = (reinterpret_cast<uintptr_t>(cache) % 16 == 0) && (reinterpret_cast<uintptr_t>(q) % 16 == 0);
   const int V = dim / 8;
@@ -192,7 +244,7 @@ void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void
     DN_CHECK(dim <= 16384, "lookup: dim too large for the scalar path");
     hipLaunchKernelGGL(scan_scalar_kernel, dim3(nb), dim3(256), dim * sizeof(float), s, q, cache, n, dim, part);
   }
-  hipLaunchKernelGGL(reduce_kernel, dim3(1), dim3(256), 0, s, part, nb, q, dim, idx_dev, score_dev);
+  hipLaunchKernelGGL(reduce_kernel, dim3(1), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out);
   DN_HIP(hipGetLastError());
 }
 
