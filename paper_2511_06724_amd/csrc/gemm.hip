@@ -267,7 +267,9 @@ template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPl
 //    the register-staged kernel.
 // Fragment-B kernel (bf16 weights in fragment order). Three tile variants share a CU
 // between several workgroups: 128 x 256 (two per CU), 128 x 128 (two) and 64 x 128
-// (four). The plan minimises a cost model fitted to measured SD-XL GEMM times on MI355X
+// (four); a five-wave 64 x 160 tile runs one workgroup per CU (linear layers only: the
+// M = 2048, N = 1280 projections are exactly one such tile per CU, where 64 x 128
+// tiles put two workgroups on a quarter of the CUs). The plan minimises a cost model fitted to measured SD-XL GEMM times on MI355X
 // (bf16, weights streamed from HBM; one fit for the linear layers, one for the implicit
 // convolutions): a run takes ceil(units / slots) rounds, a round
 // costs the MFMA work of the units resident on a CU at a per-CU rate R plus a fixed
@@ -282,9 +284,13 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
   };
   // separate fits for the linear layers and the implicit convolutions (whose A gather
   // and tap masks change the per-stage cost)
-  static const Var lin_vars[] = {{128, 256, 2, 2.4e6, 5.0, 1.0}, {128, 128, 2, 2.0e6, 8.0, 0.0}, {64, 128, 4, 1.6e6, 3.0, 0.0}};
+  static const Var lin_vars[] = {{128, 256, 2, 2.4e6, 5.0, 1.0},
+                                 {128, 128, 2, 2.0e6, 8.0, 0.0},
+                                 {64, 128, 4, 1.6e6, 3.0, 0.0},
+                                 {64, 160, 1, 3.1e6, 9.4, 0.0}};
   static const Var conv_vars[] = {{128, 256, 2, 2.4e6, 5.0, 3.0}, {128, 128, 2, 1.6e6, 1.0, 0.0}, {64, 128, 4, 1.6e6, 1.0, 0.0}};
   const Var* vars = conv ? conv_vars : lin_vars;
+  const int nvars = conv ? 3 : 4;  // the five-wave 64 x 160 tile takes linear layers only
   // convolutions: a partly filled round costs more than its average load per CU (the
   // CUs that hold one more unit finish last)
   const double fill_penalty = conv ? 0.25 : 0.0;
@@ -293,9 +299,12 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
   best.frag = 1;
   double best_t = 1e300;
   const int nk = K / 64;
-  for (int vi = 0; vi < 3; ++vi) {
+  for (int vi = 0; vi < nvars; ++vi) {
     const Var& v = vars[vi];
     if (geglu && v.bn != 256) continue;
+    // the five-wave tile wins where the fixed cost dominates (measured up to K = 2560);
+    // deeper contractions (FF-out, K = 5120) run faster as split 128 x 256 tiles
+    if (v.bn == 160 && K > 2560) continue;
     const long long tiles = (long long)ceil_div(M, v.bm) * ceil_div(N, v.bn);
     for (int sp = 1; sp <= kMaxSplit; ++sp) {
       if (sp > 1 && (geglu || !allow_split || nk / sp < 4)) break;

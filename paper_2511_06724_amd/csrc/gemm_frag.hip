@@ -36,7 +36,6 @@ namespace {
 constexpr int kXcds = 8;
 constexpr int kBK = 64;
 constexpr int kRowBytes = 128;
-constexpr int kThreads = 256;
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void gbl_void;
@@ -72,9 +71,9 @@ template <int I, int NM, int NR, int NV> struct KSched {
   }
 };
 
-template <int BM, int FN, int S> constexpr size_t frag_lds_bytes() {
+template <int BM, int FN, int S, int NW> constexpr size_t frag_lds_bytes() {
   constexpr size_t stages = size_t(S) * BM * kRowBytes;
-  constexpr size_t epi = size_t(4) * 32 * (32 * FN + 4) * 4;
+  constexpr size_t epi = size_t(NW) * 32 * (32 * FN + 4) * 4;
   return stages > epi ? stages : epi;
 }
 
@@ -84,15 +83,17 @@ template <int BM, int FN, int S> constexpr size_t frag_lds_bytes() {
 // allocation must allow (2: two workgroups share a CU, so one's prologue, barriers and
 // epilogue overlap the other's MFMAs). PRE: read a whole LDS stage of A fragments one
 // stage ahead into registers (small tiles, whose few MFMAs per k-step cannot cover an
-// LDS read latency), instead of one k-step ahead.
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_frag_kernel(
+// LDS read latency), instead of one k-step ahead. NW: waves per workgroup, each owning
+// 32 FN columns; with five (a 160-column tile) the first four issue the A DMA.
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW = 4>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_frag_kernel(
     GemmParams p, int mt, int nt, int nsplit) {
   constexpr int FM = BM / 32;
   constexpr int WN = 32 * FN;
-  constexpr int BN = 4 * WN;
+  constexpr int BN = NW * WN;
   constexpr int STAGE = BM * kRowBytes;
-  constexpr int PW = BM / 32;  // DMA instructions (8 rows of 128 B) per wave per stage
+  constexpr int PW = BM / 32;  // DMA instructions (8 rows of 128 B) per DMA wave per stage
+  static_assert(NW == 4 || NW == 5, "four or five waves");
   constexpr int NM = FM * FN;
   static_assert(D == 1 || D == 2, "one or two B buffers");
   static_assert(S >= 2 && S <= 6, "2 to 6 LDS stages");
@@ -161,7 +162,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
   const bf16* const gA0 = static_cast<const bf16*>(p.a0);
   const bf16* const gA1 = static_cast<const bf16*>(p.a1);
 
-  // DMA of A stage kt into LDS slot `slot`: PW global_load_lds per wave, no branches.
+  // DMA of A stage kt into LDS slot `slot`: PW global_load_lds per DMA wave, no branches
+  // (a fifth wave issues none).
   // Stages past this unit's range read the 16-byte zero block instead, so every
   // hand-over issues the same number of loads.
   auto issue_a = [&](int kt_in, int slot) {
@@ -179,6 +181,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WPE, W
     const bf16* a_src = second ? gA1 : gA0;
     const int a_c = second ? c - p.c0 : c;
     const int tap_off = (MODE == 2 && !p.up) ? (ky * p.in_w + kx) * p.lda0 : 0;
+    if (NW > 4 && wave >= 4) return;
 #pragma unroll
     for (int j = 0; j < PW; ++j) {
       const int q = wave * PW + j;
@@ -619,35 +622,36 @@ void splitk_reduce(const GemmParams& p, int nsplit, hipStream_t s) {
   DN_HIP(hipGetLastError());
 }
 
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE>
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW>
 void launch_frag(const GemmParams& p, int nsplit, hipStream_t s) {
-  constexpr size_t lds = frag_lds_bytes<BM, FN, S>();
+  constexpr size_t lds = frag_lds_bytes<BM, FN, S, NW>();
   static bool attr_set = false;
   if (!attr_set) {
-    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE>),
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
     attr_set = true;
   }
-  const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, 128 * FN);
-  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE>), dim3(mt * nt * nsplit), dim3(kThreads), lds,
-                     s, p, mt, nt, nsplit);
+  const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, 32 * FN * NW);
+  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW>), dim3(mt * nt * nsplit), dim3(64 * NW),
+                     lds, s, p, mt, nt, nsplit);
   DN_HIP(hipGetLastError());
 }
 
-template <int BM, int FN, int S, int D, int WPE, int MODE, int PRE = 0>
+template <int BM, int FN, int S, int D, int WPE, int MODE, int PRE = 0, int NW = 4>
 void run_frag(const GemmParams& p, int nsplit, hipStream_t s) {
   if (p.raw_partial) {
-    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE>(p, nsplit, s);
+    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE, NW>(p, nsplit, s);
   } else if (nsplit > 1) {
-    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE>(p, nsplit, s);
+    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE, NW>(p, nsplit, s);
     splitk_reduce(p, nsplit, s);
   } else {
-    launch_frag<BM, FN, S, D, WPE, MODE, false, PRE>(p, 1, s);
+    launch_frag<BM, FN, S, D, WPE, MODE, false, PRE, NW>(p, 1, s);
   }
 }
 
 // Tile plans (three LDS stages): 128 x 256 (FN = 2) with one B buffer, two workgroups per
-// CU; 128 x 128 (FN = 1) and 64 x 128 with two B buffers, two / four workgroups per CU.
+// CU; 128 x 128 (FN = 1) and 64 x 128 with two B buffers, two / four workgroups per CU;
+// 64 x 160 (five waves) with two B buffers, one workgroup per CU.
 // stages = 2 selects the 128 x 256 variant with two B buffers and one workgroup per CU.
 template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
   if (g.bm == 128 && g.bn == 256 && g.stages == 3) return run_frag<128, 2, 3, 1, 2, MODE>(p, g.split, s);
@@ -659,6 +663,9 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   if (g.bm == 128 && g.bn == 128 && g.stages == 13) return run_frag<128, 1, 3, 2, 2, MODE, 1>(p, g.split, s);
   if (g.bm == 64 && g.bn == 256 && g.stages == 13) return run_frag<64, 2, 3, 2, 2, MODE, 1>(p, g.split, s);
   if (g.bm == 32 && g.bn == 128 && g.stages == 13) return run_frag<32, 1, 3, 2, 4, MODE, 1>(p, g.split, s);
+  if constexpr (MODE != 2) {
+    if (g.bm == 64 && g.bn == 160 && g.stages == 3) return run_frag<64, 1, 3, 2, 2, MODE, 0, 5>(p, g.split, s);
+  }
   throw Error(-1, "gemm: no fragment-B kernel for this tile plan");
 }
 
