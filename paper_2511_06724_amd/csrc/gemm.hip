@@ -267,9 +267,11 @@ template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPl
 //    the register-staged kernel.
 // Fragment-B kernel (bf16 weights in fragment order). Three tile variants share a CU
 // between several workgroups: 128 x 256 (two per CU), 128 x 128 (two) and 64 x 128
-// (four); a five-wave 64 x 160 tile runs one workgroup per CU (linear layers only: the
-// M = 2048, N = 1280 projections are exactly one such tile per CU, where 64 x 128
-// tiles put two workgroups on a quarter of the CUs). The plan minimises a cost model fitted to measured SD-XL GEMM times on MI355X
+// (four); five-wave 64 x 160 and 128 x 160 tiles run one workgroup per CU (the M = 2048,
+// N = 1280 projections are exactly one 64 x 160 tile per CU, where 64 x 128 tiles put
+// two workgroups on a quarter of the CUs; 128 x 160 tiles cover the 8192-row N = 640
+// layers in one round and the N = 320 convolutions without padding columns). The plan
+// minimises a cost model fitted to measured SD-XL GEMM times on MI355X
 // (bf16, weights streamed from HBM; one fit for the linear layers, one for the implicit
 // convolutions): a run takes ceil(units / slots) rounds, a round
 // costs the MFMA work of the units resident on a CU at a per-CU rate R plus a fixed
@@ -287,10 +289,14 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
   static const Var lin_vars[] = {{128, 256, 2, 2.4e6, 5.0, 1.0},
                                  {128, 128, 2, 2.0e6, 8.0, 0.0},
                                  {64, 128, 4, 1.6e6, 3.0, 0.0},
-                                 {64, 160, 1, 3.1e6, 9.4, 0.0}};
-  static const Var conv_vars[] = {{128, 256, 2, 2.4e6, 5.0, 3.0}, {128, 128, 2, 1.6e6, 1.0, 0.0}, {64, 128, 4, 1.6e6, 1.0, 0.0}};
+                                 {64, 160, 1, 3.1e6, 9.4, 0.0},
+                                 {128, 160, 1, 4.14e6, 16.7, 0.0}};
+  static const Var conv_vars[] = {{128, 256, 2, 2.4e6, 5.0, 3.0},
+                                  {128, 128, 2, 1.6e6, 1.0, 0.0},
+                                  {64, 128, 4, 1.6e6, 1.0, 0.0},
+                                  {128, 160, 1, 3.39e6, 10.7, 0.0}};
   const Var* vars = conv ? conv_vars : lin_vars;
-  const int nvars = conv ? 3 : 4;  // the five-wave 64 x 160 tile takes linear layers only
+  const int nvars = conv ? 4 : 5;  // the five-wave 64 x 160 tile takes linear layers only
   // convolutions: a partly filled round costs more than its average load per CU (the
   // CUs that hold one more unit finish last)
   const double fill_penalty = conv ? 0.25 : 0.0;
@@ -307,7 +313,8 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
     if (v.bn == 160 && K > 2560) continue;
     const long long tiles = (long long)ceil_div(M, v.bm) * ceil_div(N, v.bn);
     for (int sp = 1; sp <= kMaxSplit; ++sp) {
-      if (sp > 1 && (geglu || !allow_split || nk / sp < 4)) break;
+      // the five-wave tiles (one workgroup per CU) were measured unsplit only
+      if (sp > 1 && (geglu || !allow_split || nk / sp < 4 || v.wg == 1)) break;
       const long long units = tiles * sp;
       const long long slots = (long long)cus * v.wg;
       const long long rounds = (units + slots - 1) / slots;

@@ -651,7 +651,7 @@ void run_frag(const GemmParams& p, int nsplit, hipStream_t s) {
 
 // Tile plans (three LDS stages): 128 x 256 (FN = 2) with one B buffer, two workgroups per
 // CU; 128 x 128 (FN = 1) and 64 x 128 with two B buffers, two / four workgroups per CU;
-// 64 x 160 (five waves) with two B buffers, one workgroup per CU.
+// 64 x 160 and 128 x 160 (five waves) with two B buffers, one workgroup per CU.
 // stages = 2 selects the 128 x 256 variant with two B buffers and one workgroup per CU.
 template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
   if (g.bm == 128 && g.bn == 256 && g.stages == 3) return run_frag<128, 2, 3, 1, 2, MODE>(p, g.split, s);
@@ -666,6 +666,7 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   if constexpr (MODE != 2) {
     if (g.bm == 64 && g.bn == 160 && g.stages == 3) return run_frag<64, 1, 3, 2, 2, MODE, 0, 5>(p, g.split, s);
   }
+  if (g.bm == 128 && g.bn == 160 && g.stages == 3) return run_frag<128, 1, 3, 2, 2, MODE, 0, 5>(p, g.split, s);
   throw Error(-1, "gemm: no fragment-B kernel for this tile plan");
 }
 

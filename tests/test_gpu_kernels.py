@@ -35,14 +35,14 @@ def _rng(seed):
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280),
                                    (2048, 2048, 128), (8192, 512, 256), (300, 1280, 2560), (77, 96, 1920),
-                                   (1000, 640, 5120), (129, 256, 704), (2000, 1248, 1280)])
+                                   (1000, 640, 5120), (129, 256, 704), (2000, 1248, 1280), (8000, 608, 2560)])
 def test_linear(dtype, M, N, K):
     """Shapes cover every tile plan: in fp32 the register-staged 64 x 64 / 128 x 128
     tiles; in bf16 the row-major kernels for N % 32 != 0 (N = 200) and the fragment-B
     kernel with 128 x 128 and 128 x 256 tiles, with and without split-K (few tiles and
-    long K: 300 x 1280 x 2560, 1000 x 640 x 5120), the five-wave 64 x 160 tile
-    (2000 x 1248 x 1280: one tile per CU, ragged last row tile and column tile), ragged
-    M and N tails."""
+    long K: 300 x 1280 x 2560, 1000 x 640 x 5120), the five-wave 64 x 160 and 128 x 160
+    tiles (2000 x 1248 x 1280, 8000 x 608 x 2560: one tile per CU, ragged last row tile
+    and column tile), ragged M and N tails."""
     announce(f"linear dtype={dtype} M={M} N={N} K={K}")
     r = _rng(M + N + K)
     x, xh = to_dev(r.standard_normal((M, K)), dtype)
