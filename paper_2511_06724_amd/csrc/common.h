@@ -75,6 +75,24 @@ __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
 }
+
+// The same sum with DPP lane moves (no LDS crossbar round trips), wave-uniform result:
+// quad butterflies, then the half-row and row mirrors give every lane its 16-lane row
+// sum; row broadcasts of lane 15 and lane 31 fold the rows into lane 63, which is read
+// back. A fixed association, so the result is deterministic.
+template <int CTRL, int ROW_MASK> __device__ __forceinline__ float dpp_add(float v) {
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROW_MASK,
+                                                                       0xf, false));
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  v = dpp_add<0xb1, 0xf>(v);   // quad_perm [1, 0, 3, 2]
+  v = dpp_add<0x4e, 0xf>(v);   // quad_perm [2, 3, 0, 1]
+  v = dpp_add<0x141, 0xf>(v);  // row_half_mirror
+  v = dpp_add<0x140, 0xf>(v);  // row_mirror
+  v = dpp_add<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+  v = dpp_add<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

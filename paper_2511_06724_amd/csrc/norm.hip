@@ -256,9 +256,10 @@ template <> struct Store4<float> {
 // x[row] = (resid ? x[row] : 0) + bias + sum_s part[s][row] in that order (the reduction of
 // a split-K GEMM that wrote fp32 partial slabs), and written back; then
 // y = (x - mean) * rstd * gamma + beta with two-pass mean / variance. Every load of the
-// row (x, the slabs, the bias) is issued before the first use, so a row waits on one
-// memory latency; vector columns past C are skipped wave-uniformly, lanes past C read a
-// valid column and are masked.
+// row (x, the slabs, the bias; gamma and beta too when NS = 0) is issued before the first
+// use, so a row waits on one memory latency; the two wave sums use DPP lane moves;
+// vector columns past C are skipped wave-uniformly, lanes past C read a valid column and
+// are masked.
 template <typename T, int NS>
 __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, int C, const float* gamma,
                                                  const float* beta, float eps, const float* part, long long slab,
@@ -272,14 +273,24 @@ __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, in
   float4 v[kLnMaxVec];
   float4 sl[NS > 0 ? NS : 1][kLnMaxVec];
   float4 bv[kLnMaxVec];
+  // the plain LayerNorm also loads gamma and beta with the row (the slab-summing
+  // variant keeps its registers for the slabs and loads them after the statistics)
+  float4 gv[NS == 0 ? kLnMaxVec : 1], btv[NS == 0 ? kLnMaxVec : 1];
+  const float4* g4 = reinterpret_cast<const float4*>(gamma);
+  const float4* b4 = reinterpret_cast<const float4*>(beta);
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
     v[j] = bv[j] = zero4;
+    if constexpr (NS == 0) gv[j] = btv[j] = zero4;
 #pragma unroll
     for (int k = 0; k < (NS > 0 ? NS : 1); ++k) sl[k][j] = zero4;
     if (64 * j < nv) {
       const int i = min(lane + 64 * j, nv - 1);
       if (NS == 0 || resid) v[j] = xr[i];
+      if constexpr (NS == 0) {
+        gv[j] = g4[i];
+        btv[j] = b4[i];
+      }
       if constexpr (NS > 0) {
         if (bias) bv[j] = reinterpret_cast<const float4*>(bias)[i];
         const float4* pr = reinterpret_cast<const float4*>(part + row * C);
@@ -314,7 +325,7 @@ __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, in
       if (i < nv) s += (v[j].x + v[j].y) + (v[j].z + v[j].w);
     }
   }
-  const float mean = wave_sum(s) / C;
+  const float mean = wave_sum_dpp(s) / C;
   float q = 0.f;
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
@@ -324,15 +335,20 @@ __global__ __launch_bounds__(256) void ln_kernel(float* x, T* y, long long M, in
       q += (a * a + b * b) + (c * c + d * d);
     }
   }
-  const float rstd = rsqrtf(wave_sum(q) / C + eps);
+  const float rstd = rsqrtf(wave_sum_dpp(q) / C + eps);
   T* yr = y + row * C;
-  const float4* g4 = reinterpret_cast<const float4*>(gamma);
-  const float4* b4 = reinterpret_cast<const float4*>(beta);
 #pragma unroll
   for (int j = 0; j < kLnMaxVec; ++j) {
     const int i = lane + 64 * j;
     if (64 * j < nv && i < nv) {
-      const float4 g = g4[i], bb = b4[i];
+      float4 g, bb;
+      if constexpr (NS == 0) {
+        g = gv[j];
+        bb = btv[j];
+      } else {
+        g = g4[i];
+        bb = b4[i];
+      }
       Store4<T>::st(yr + 4 * i, (v[j].x - mean) * rstd * g.x + bb.x, (v[j].y - mean) * rstd * g.y + bb.y,
                     (v[j].z - mean) * rstd * g.z + bb.z, (v[j].w - mean) * rstd * g.w + bb.w);
     }
