@@ -268,6 +268,7 @@ __global__ __launch_bounds__(64 * NQ) __attribute__((amdgpu_waves_per_eu(WPE, WP
   constexpr int PW = TI / NQ;                // per wave per tile
   constexpr int U = R % 2 == 0 ? R : 2 * R;  // unroll: ring slot and score buffer fixed
   static_assert(TI % NQ == 0, "DMA instructions must divide over the waves");
+  static_assert((kKT / 8) % PW == 0, "a wave's DMA rows must be all K rows or all V^T rows (two or more waves)");
   static_assert(R >= (PIPE ? 3 : 2) && R <= 5, "ring of 3 (2 without score read-ahead) to 5 tiles");
 
   extern __shared__ __align__(16) unsigned char smem[];
