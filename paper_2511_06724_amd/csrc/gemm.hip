@@ -308,9 +308,9 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
   for (int vi = 0; vi < nvars; ++vi) {
     const Var& v = vars[vi];
     if (geglu && v.bn != 256) continue;
-    // the five-wave tile wins where the fixed cost dominates (measured up to K = 2560);
-    // deeper contractions (FF-out, K = 5120) run faster as split 128 x 256 tiles
-    if (v.bn == 160 && K > 2560) continue;
+    // the five-wave 64 x 160 tile wins where the fixed cost dominates (measured up to
+    // K = 2560); deeper contractions (FF-out, K = 5120) run faster as split 128 x 256 tiles
+    if (v.bm == 64 && v.bn == 160 && K > 2560) continue;
     const long long tiles = (long long)ceil_div(M, v.bm) * ceil_div(N, v.bn);
     for (int sp = 1; sp <= kMaxSplit; ++sp) {
       // the five-wave tiles (one workgroup per CU) were measured unsplit only
