@@ -2,16 +2,18 @@
 //
 // Same contraction and epilogue as gemm.hip (see kernels.h), organised for the
 // dense bf16 hot path:
-//  - B, the packed weight matrix, is stored in MFMA fragment order (gemm_frag_index):
+//  - B, the packed weight matrix, is stored in MFMA fragment order (to_frag, below):
 //    for each block of 32 output columns and each k-step of 16, the 64 lanes' 16-byte
 //    operands lie in 1 KB of contiguous memory. Each wave loads its own B fragments
-//    with one coalesced 16-byte load per lane straight into registers, two LDS stages
-//    ahead, so B costs no LDS bandwidth;
+//    with one coalesced 16-byte load per lane straight into registers, one or two LDS
+//    stages ahead, so B costs no LDS bandwidth;
 //  - A (the activations, or the implicit-convolution gather) goes global -> LDS with
 //    global_load_lds_dwordx4 into S stages of BK = 64 (128-byte rows, chunk c of row r
-//    at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1)), shared by the 4 waves;
-//  - block tile BM x 4 * 32 FN: the 4 waves split the columns, each computes BM x 32 FN
-//    with 32x32x16 MFMAs issued as C^T = B A^T (four consecutive output columns per lane);
+//    at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1)), shared by the waves (four
+//    issue the loads);
+//  - block tile BM x NW * 32 FN: the NW (4 or 5) waves split the columns, each computes
+//    BM x 32 FN with 32x32x16 MFMAs issued as C^T = B A^T (four consecutive output
+//    columns per lane);
 //  - every k-step interleaves one MFMA, one LDS fragment read for the next k-step and
 //    its share of B loads (scheduling groups); the stage hand-over (wait + barrier)
 //    sits before the last k-step, whose MFMAs cover the first reads of the next stage;
