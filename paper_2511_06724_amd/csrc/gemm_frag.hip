@@ -546,38 +546,55 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
       }
     } else {
       // GEGLU: within each 64-column pair block, columns [0, 32) are values and
-      // [32, 64) the matching gates; output column = (pair block) * 32 + c. A lane's
-      // value and gate columns are the same in every pass: their biases load once.
-      constexpr int LPR = WN / 8;
-      constexpr int RPI = 64 / LPR;
-      const int cq = (lane % LPR) * 4;            // 0 .. WN/2 - 4
-      const int pb = cq / 32, c4 = cq % 32;       // pair block, column in it
-      const int lc = pb * 64 + c4;                // value column within the wave
-      const int nv = nw0 + lc;
-      const int o = nw0 / 2 + cq;
-      float ba[4] = {0.f, 0.f, 0.f, 0.f}, bg[4] = {0.f, 0.f, 0.f, 0.f};
-      if (p.bias && o < p.n_store) {
+      // [32, 64) the matching gates; output column = (pair block) * 32 + c. A lane takes
+      // 8 consecutive outputs of a row, so each store is 16 bytes (4 lanes cover a row's
+      // 64-byte segment); its value and gate columns are the same in every pass, so
+      // their biases load once.
+      // (tiles with 32 columns per wave never take GEGLU: the host rejects them)
+      if constexpr (WN % 64 == 0) {
+        constexpr int LPR = WN / 16;
+        constexpr int RPI = 64 / LPR;
+        const int cq = (lane % LPR) * 8;            // 0 .. WN/2 - 8
+        const int pb = cq / 32, c8 = cq % 32;       // pair block, column in it
+        const int lc = pb * 64 + c8;                // value column within the wave
+        const int nv = nw0 + lc;
+        const int o = nw0 / 2 + cq;
+        float ba[8], bg[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          ba[e] = p.bias[nv + e];
-          bg[e] = p.bias[nv + 32 + e];
+        for (int e = 0; e < 8; ++e) ba[e] = bg[e] = 0.f;
+        if (p.bias && o < p.n_store) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            ba[e] = p.bias[nv + e];
+            bg[e] = p.bias[nv + 32 + e];
+          }
         }
-      }
+        const bool vec8 = !p.out_f32 && o + 8 <= p.n_store && (p.ldo & 7) == 0;
 #pragma unroll
-      for (int t = 0; t < 32 / RPI; ++t) {
-        const int rr = t * RPI + lane / LPR;
-        const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc);
-        const f32x4 g4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 32);
-        const int m = mb + rr;
-        if (m >= p.M || o >= p.n_store) continue;
-        float v[4];
+        for (int t = 0; t < 32 / RPI; ++t) {
+          const int rr = t * RPI + lane / LPR;
+          const f32x4 a0 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc);
+          const f32x4 a1 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 4);
+          const f32x4 g0 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 32);
+          const f32x4 g1 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 36);
+          const int m = mb + rr;
+          if (m >= p.M || o >= p.n_store) continue;
+          float v[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float a = a4[e] + ba[e];
-          const float gg = g4[e] + bg[e];
-          v[e] = a * gelu_erf(gg);
+          for (int e = 0; e < 4; ++e) {
+            v[e] = (a0[e] + ba[e]) * gelu_erf(g0[e] + bg[e]);
+            v[e + 4] = (a1[e] + ba[e + 4]) * gelu_erf(g1[e] + bg[e + 4]);
+          }
+          if (vec8) {
+            bf16x8 w;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) w[e] = static_cast<bf16>(v[e]);
+            *reinterpret_cast<bf16x8*>(static_cast<bf16*>(p.out) + (long long)m * p.ldo + o) = w;
+          } else {
+            store4<bf16>(p, m, o, v, p.n_store);
+            store4<bf16>(p, m, o + 4, v + 4, p.n_store);
+          }
         }
-        store4<bf16>(p, m, o, v, p.n_store);
       }
     }
   }
