@@ -73,6 +73,67 @@ template <int I, int NM, int NR, int NV> struct KSched {
   }
 };
 
+// Epilogue inputs and outputs of 8 consecutive columns [n, n + 8) of row m (n % 8 == 0).
+// The 16-byte forms need the whole group inside n_store, a leading dimension that keeps
+// every row's group 16-byte aligned and a 16-byte aligned base; otherwise element-wise,
+// with zeros (loads) or nothing (stores) past n_store.
+__device__ __forceinline__ bool aligned16(const void* q) {
+  return (reinterpret_cast<__UINTPTR_TYPE__>(q) & 15) == 0;
+}
+__device__ __forceinline__ bool resid_vec8(const GemmParams& p) {
+  return aligned16(p.resid) && (p.ldr & (p.resid_f32 ? 3 : 7)) == 0;
+}
+__device__ __forceinline__ bool out_vec8(const GemmParams& p) {
+  return aligned16(p.out) && (p.ldo & (p.out_f32 ? 3 : 7)) == 0;
+}
+__device__ __forceinline__ void load_rowvec8(const GemmParams& p, int m, int n, float v[8]) {
+  const float* r = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = n + e < p.n_store ? r[e] : 0.f;
+}
+__device__ __forceinline__ void load_resid8(const GemmParams& p, int m, int n, bool vec, float v[8]) {
+  const long long ro = (long long)m * p.ldr + n;
+  if (vec) {
+    if (p.resid_f32) {
+      const f32x4* r = reinterpret_cast<const f32x4*>(static_cast<const float*>(p.resid) + ro);
+      const f32x4 a = r[0], b = r[1];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] = a[e];
+        v[e + 4] = b[e];
+      }
+    } else {
+      const bf16x8 r = *reinterpret_cast<const bf16x8*>(static_cast<const bf16*>(p.resid) + ro);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = static_cast<float>(r[e]);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      v[e] = n + e >= p.n_store ? 0.f
+             : p.resid_f32      ? static_cast<const float*>(p.resid)[ro + e]
+                                : static_cast<float>(static_cast<const bf16*>(p.resid)[ro + e]);
+  }
+}
+__device__ __forceinline__ void store8(const GemmParams& p, int m, int n, const float v[8], bool vec) {
+  const long long o = (long long)m * p.ldo + n;
+  if (vec) {
+    if (p.out_f32) {
+      f32x4* d = reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + o);
+      d[0] = f32x4{v[0], v[1], v[2], v[3]};
+      d[1] = f32x4{v[4], v[5], v[6], v[7]};
+    } else {
+      bf16x8 w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[e] = static_cast<bf16>(v[e]);
+      *reinterpret_cast<bf16x8*>(static_cast<bf16*>(p.out) + o) = w;
+    }
+  } else {
+    store4<bf16>(p, m, n, v, p.n_store);
+    store4<bf16>(p, m, n + 4, v + 4, p.n_store);
+  }
+}
+
 template <int BM, int FN, int S, int NW> constexpr size_t frag_lds_bytes() {
   constexpr size_t stages = size_t(S) * BM * kRowBytes;
   constexpr size_t epi = size_t(NW) * 32 * (32 * FN + 4) * 4;
@@ -233,50 +294,34 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   // Epilogue input of the plain path (the residual or the per-sample row vector, when
   // exactly one is present) for small wave tiles of the linear modes without stage
   // read-ahead (where the registers are free): loaded before the main loop, whose
-  // latency then hides the load, into FM x ENP 16-byte registers per lane.
-  constexpr int ELPR = WN / 4;     // lanes per row in the row-contiguous epilogue
+  // latency then hides the load, into FM x ENP x 2 16-byte registers per lane, in the
+  // layout of the row-contiguous epilogue (8 consecutive columns per lane).
+  constexpr int ELPR = WN / 8;     // lanes per row in the row-contiguous epilogue
   constexpr int ERPI = 64 / ELPR;  // rows per pass
   constexpr int ENP = 32 / ERPI;   // passes per 32-row block
-  constexpr bool kPreIn = !SPLIT && !PRE && MODE != 2 && FM * ENP * 4 <= 32;
+  constexpr bool kPreIn = !SPLIT && !PRE && MODE != 2 && FM * ENP * 8 <= 32;
   const int enw0 = n0 + wave * WN;
   const bool pre_in = kPreIn && !p.geglu && !(p.vt && enw0 + WN > p.vt_col0) &&
                       ((p.resid != nullptr) != (p.rowvec != nullptr));
-  f32x4 pin[kPreIn ? FM : 1][kPreIn ? ENP : 1];
+  f32x4 pin[kPreIn ? FM : 1][kPreIn ? ENP : 1][2];
   if constexpr (kPreIn) {
     if (pre_in) {
-      const int n = enw0 + (lane % ELPR) * 4;
-      const bool full = n + 4 <= p.n_store;
+      const int n = enw0 + (lane % ELPR) * 8;
+      const bool rvec = n + 8 <= p.n_store && p.resid && resid_vec8(p);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int t = 0; t < ENP; ++t) {
           const int m = m0 + i * 32 + t * ERPI + lane / ELPR;
-          f32x4 v = {0.f, 0.f, 0.f, 0.f};
+          float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
           if (m < p.M && n < p.n_store) {
-            if (p.rowvec) {
-              const float* r = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
-#pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = (full || n + e < p.n_store) ? r[e] : 0.f;
-            } else {
-              const long long ro = (long long)m * p.ldr + n;
-              if (full && (p.ldr & 3) == 0) {
-                if (p.resid_f32) {
-                  v = *reinterpret_cast<const f32x4*>(static_cast<const float*>(p.resid) + ro);
-                } else {
-                  const bf16x4 r = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(p.resid) + ro);
-#pragma unroll
-                  for (int e = 0; e < 4; ++e) v[e] = static_cast<float>(r[e]);
-                }
-              } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  if (n + e < p.n_store)
-                    v[e] = p.resid_f32 ? static_cast<const float*>(p.resid)[ro + e]
-                                       : static_cast<float>(static_cast<const bf16*>(p.resid)[ro + e]);
-              }
-            }
+            if (p.rowvec)
+              load_rowvec8(p, m, n, v);
+            else
+              load_resid8(p, m, n, rvec, v);
           }
-          pin[i][t] = v;
+          pin[i][t][0] = f32x4{v[0], v[1], v[2], v[3]};
+          pin[i][t][1] = f32x4{v[4], v[5], v[6], v[7]};
         }
     }
   }
@@ -473,68 +518,47 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
         *reinterpret_cast<f32x4*>(slab + (long long)m * p.n_store + n) = v4;
       }
     } else if (!p.geglu) {
-      // A lane's 4 columns are the same in every pass; the row vector and residual of
+      // A lane takes 8 consecutive columns of a row (16-byte bf16 stores: 4 lanes cover
+      // a row's 64-byte segment), the same in every pass; the row vector and residual of
       // every pass of this 32-row block are loaded before the block is read back from
       // LDS, so the block waits on one memory latency instead of one per pass. Same
       // arithmetic as epilogue_group: ((acc + bias) + row vector) + residual.
-      constexpr int LPR = WN / 4;
+      constexpr int LPR = WN / 8;
       constexpr int RPI = 64 / LPR;
       constexpr int NP = 32 / RPI;
-      const int c4 = (lane % LPR) * 4;
-      const int n = nw0 + c4;
+      const int c8 = (lane % LPR) * 8;
+      const int n = nw0 + c8;
       const bool ncol = n < p.n_store;
-      const bool full = n + 4 <= p.n_store;
-      float rv[NP][4], rs[NP][4];
+      const bool full = n + 8 <= p.n_store;
+      const bool rvec = full && p.resid && resid_vec8(p);
+      float rv[NP][8], rs[NP][8];
 #pragma unroll
       for (int t = 0; t < NP; ++t) {
         const int m = mb + t * RPI + lane / LPR;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) rv[t][e] = rs[t][e] = 0.f;
+        for (int e = 0; e < 8; ++e) rv[t][e] = rs[t][e] = 0.f;
         if (m >= p.M || !ncol || pre_in) continue;
-        if (p.rowvec) {
-          const float* r = p.rowvec + (long long)(m / p.rows_per_sample) * p.rowvec_ld + n;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) rv[t][e] = (full || n + e < p.n_store) ? r[e] : 0.f;
-        }
-        if (p.resid) {
-          const long long ro = (long long)m * p.ldr + n;
-          if (full && (p.ldr & 3) == 0) {
-            if (p.resid_f32) {
-              const f32x4 r = *reinterpret_cast<const f32x4*>(static_cast<const float*>(p.resid) + ro);
-#pragma unroll
-              for (int e = 0; e < 4; ++e) rs[t][e] = r[e];
-            } else {
-              const bf16x4 r = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(p.resid) + ro);
-#pragma unroll
-              for (int e = 0; e < 4; ++e) rs[t][e] = static_cast<float>(r[e]);
-            }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (n + e < p.n_store)
-                rs[t][e] = p.resid_f32 ? static_cast<const float*>(p.resid)[ro + e]
-                                       : static_cast<float>(static_cast<const bf16*>(p.resid)[ro + e]);
-          }
-        }
+        if (p.rowvec) load_rowvec8(p, m, n, rv[t]);
+        if (p.resid) load_resid8(p, m, n, rvec, rs[t]);
       }
-      float bias4[4] = {0.f, 0.f, 0.f, 0.f};
-      if (p.bias && ncol) {
+      float bias8[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) bias4[e] = (full || n + e < p.n_store) ? p.bias[n + e] : 0.f;
-      }
+      for (int e = 0; e < 8; ++e) bias8[e] = p.bias && n + e < p.n_store ? p.bias[n + e] : 0.f;
+      const bool ovec = full && out_vec8(p);
 #pragma unroll
       for (int t = 0; t < NP; ++t) {
         const int rr = t * RPI + lane / LPR;
-        const f32x4 v4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c4);
+        const f32x4 a0 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c8);
+        const f32x4 a1 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c8 + 4);
         const int m = mb + rr;
         if (m >= p.M || !ncol) continue;
-        float v[4];
+        float v[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float x = v4[e];
-          if (p.bias) x += bias4[e];
+        for (int e = 0; e < 8; ++e) {
+          float x = e < 4 ? a0[e] : a1[e - 4];
+          if (p.bias) x += bias8[e];
           if constexpr (kPreIn) {
-            if (pre_in) x += pin[i][t][e];
+            if (pre_in) x += pin[i][t][e / 4][e % 4];
           }
           if (!pre_in) {
             if (p.rowvec) x += rv[t][e];
@@ -542,7 +566,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
           }
           v[e] = x;
         }
-        store4<bf16>(p, m, n, v, p.n_store);
+        store8(p, m, n, v, ovec);
       }
     } else {
       // GEGLU: within each 64-column pair block, columns [0, 32) are values and
@@ -569,7 +593,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
             bg[e] = p.bias[nv + 32 + e];
           }
         }
-        const bool vec8 = !p.out_f32 && o + 8 <= p.n_store && (p.ldo & 7) == 0;
+        const bool vec8 = !p.out_f32 && o + 8 <= p.n_store && out_vec8(p);
 #pragma unroll
         for (int t = 0; t < 32 / RPI; ++t) {
           const int rr = t * RPI + lane / LPR;

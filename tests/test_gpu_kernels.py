@@ -42,7 +42,8 @@ def test_linear(dtype, M, N, K):
     kernel with 128 x 128 and 128 x 256 tiles, with and without split-K (few tiles and
     long K: 300 x 1280 x 2560, 1000 x 640 x 5120), the five-wave 64 x 160 and 128 x 160
     tiles (2000 x 1248 x 1280, 8000 x 608 x 2560: one tile per CU, ragged last row tile
-    and column tile), ragged M and N tails."""
+    and column tile), ragged M and N tails. Outputs: bf16 / fp32 without residual, fp32
+    with an fp32 residual, and the op's dtype with a residual in that dtype."""
     announce(f"linear dtype={dtype} M={M} N={N} K={K}")
     r = _rng(M + N + K)
     x, xh = to_dev(r.standard_normal((M, K)), dtype)
@@ -54,10 +55,14 @@ def test_linear(dtype, M, N, K):
     dn.op_linear(dtype, x, wp, f32_dev(b), y, M, N, K)
     yr = torch.empty((M, N), device=DEV, dtype=torch.float32)
     dn.op_linear(dtype, x, wp, f32_dev(b), yr, M, N, K, resid=f32_dev(res), resid_f32=True, y_f32=True)
+    resd, resh = to_dev(res, dtype)
+    yd = torch.empty((M, N), device=DEV, dtype=tdtype(dtype))
+    dn.op_linear(dtype, x, wp, f32_dev(b), yd, M, N, K, resid=resd)
     torch.cuda.synchronize()
     ref = L.linear(xh, wh, b.astype(np.float64))
     assert rel_l2(host(y), ref) < TOL[dtype]
     assert rel_l2(host(yr), ref + res) < (1e-5 if dtype == dn.DN_FP32 else 2e-3)
+    assert rel_l2(host(yd), ref + resh) < TOL[dtype]
 
 
 def _interleave(w1, n):
