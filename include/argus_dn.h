@@ -14,6 +14,7 @@
  *   dn_create                          build a denoiser (pack weights for the GPU)
  *   dn_denoise                         run iterations [start_step, start_step + n_steps)
  *   ac_lookup                          top-1 cosine search over the prompt-embedding cache
+ *   ac_lookup_batch                    the same search for many queries in one pass over the cache
  *   ac_fetch_latent                    copy cached latent #idx into an fp32 latent buffer
  *   dn_unet_eps                        one UNet evaluation + guidance (per-step check hook)
  *   dn_op_*                            single-kernel entry points (kernel checks, timing)
@@ -195,6 +196,21 @@ dn_status dn_unet_eps(dn_handle* h, const float* x, int32_t t, const float* text
  * on them. */
 dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64_t n, int32_t dim,
                     int64_t* out_idx, float* out_score);
+
+/* Batched nearest cached prompt (Sec. 2.1; Sec. 4.7): for each of the nq queries
+ * of query_embs (device fp16 [nq][dim], row-major) the same search as ac_lookup
+ * over cache_embs (device fp16 [n][dim]): out_idx[j] (host int64 [nq]) receives
+ * the first row of maximal cosine with query j, or -1 when query j is zero (or
+ * every row is), and out_score[j] (host float [nq], may be NULL) that cosine.
+ * For dim 256, 512, 768 or 1024 with 16-byte aligned pointers the table is read
+ * once per 64 queries and the scores are matrix-core products (fp16 operands,
+ * fp32 sums); other widths run one ac_lookup scan per query. Synchronous (default
+ * stream). nq >= 1, n >= 1, dim >= 1; on an argument error nothing is written.
+ * The first call on a device allocates that device's workspace (256 KB) and a
+ * 768-byte pinned host result buffer, kept until the process ends; calls that
+ * overlap on one device race on them. */
+dn_status ac_lookup_batch(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n, int32_t dim,
+                          int64_t* out_idx, float* out_score);
 
 /* Copies cached latent #idx of a device bf16 table [n][numel] into the device
  * fp32 latent buffer [numel] (the resume state of Sec. 4.7). Asynchronous. */

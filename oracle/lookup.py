@@ -39,3 +39,36 @@ def top2_gap(query, cache):
         return float("inf")
     a = np.partition(s, -2)[-2:]
     return float(a[1] - a[0])
+
+
+def cosine_scores_batch(queries, cache):
+    """fp64 cosine similarity of every query row [nq, dim] against every cache row
+    [n, dim]: [nq, n]. Zero-norm rows score -inf; a zero query's row is all nan."""
+    q = np.atleast_2d(np.asarray(queries, dtype=np.float64))
+    c = np.asarray(cache, dtype=np.float64)
+    cn = np.linalg.norm(c, axis=1)
+    qn = np.linalg.norm(q, axis=1)
+    out = np.full((q.shape[0], c.shape[0]), -np.inf)
+    ok = cn > 0
+    out[:, ok] = (q @ c[ok].T) / cn[ok][None, :]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        out = out / qn[:, None]
+    out[qn == 0] = np.nan
+    return out
+
+
+def top1_batch(queries, cache):
+    """Batched search (approximate caching serves many prompts against one cache,
+    Sec. 2.1; Sec. 4.5): for every query row, the row of maximal cosine exactly as
+    `top1`, ties to the lowest index. A zero query has no defined cosine and gets
+    (-1, nan); so does a query against a cache of zero rows only.
+    Returns (indices [nq] int64, scores [nq] fp64)."""
+    s = cosine_scores_batch(queries, cache)
+    idx = np.full(s.shape[0], -1, np.int64)
+    score = np.full(s.shape[0], np.nan)
+    for j in range(s.shape[0]):
+        if not np.isfinite(s[j]).any():
+            continue
+        idx[j] = int(np.argmax(s[j]))
+        score[j] = float(s[j, idx[j]])
+    return idx, score

@@ -46,6 +46,8 @@ struct LookupWs {
   std::mutex mu;
   std::vector<void*> ws;
   std::vector<LookupRes*> res;
+  std::vector<void*> batch_ws;        // per-workgroup winners of the batched scan
+  std::vector<long long*> batch_res;  // pinned: 64 indices, then 64 scores
 };
 LookupWs g_lookup;
 
@@ -59,6 +61,21 @@ void lookup_state(int dev, void** ws, LookupRes** res) {
   if (!g_lookup.res[dev]) DN_HIP(hipHostMalloc(reinterpret_cast<void**>(&g_lookup.res[dev]), 256));
   *ws = g_lookup.ws[dev];
   *res = g_lookup.res[dev];
+}
+
+void lookup_batch_state(int dev, void** ws, long long** idx, float** score) {
+  std::lock_guard<std::mutex> lk(g_lookup.mu);
+  if ((int)g_lookup.batch_ws.size() <= dev) {
+    g_lookup.batch_ws.resize(dev + 1, nullptr);
+    g_lookup.batch_res.resize(dev + 1, nullptr);
+  }
+  const int mq = dn::lookup_batch_max_queries();
+  if (!g_lookup.batch_ws[dev]) DN_HIP(hipMalloc(&g_lookup.batch_ws[dev], dn::lookup_batch_workspace_bytes()));
+  if (!g_lookup.batch_res[dev])
+    DN_HIP(hipHostMalloc(reinterpret_cast<void**>(&g_lookup.batch_res[dev]), mq * (sizeof(long long) + sizeof(float))));
+  *ws = g_lookup.batch_ws[dev];
+  *idx = g_lookup.batch_res[dev];
+  *score = reinterpret_cast<float*>(g_lookup.batch_res[dev] + mq);
 }
 
 bool is_dtype(int32_t d) { return d == DN_FP32 || d == DN_BF16; }
@@ -195,6 +212,50 @@ dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64
     DN_CHECK(idx >= 0 && idx < n, "ac_lookup: no row scored (zero query or zero-norm cache)");
     *out_idx = idx;
     if (out_score) *out_score = score;
+  });
+}
+
+dn_status ac_lookup_batch(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n, int32_t dim,
+                          int64_t* out_idx, float* out_score) {
+  return guarded([&] {
+    DN_CHECK(query_embs && cache_embs && out_idx, "ac_lookup_batch: null pointer");
+    DN_CHECK(nq >= 1, "ac_lookup_batch: nq must be >= 1");
+    DN_CHECK(n >= 1, "ac_lookup_batch: n must be >= 1");
+    DN_CHECK(dim >= 1, "ac_lookup_batch: dim must be >= 1");
+    int dev = 0;
+    DN_HIP(hipGetDevice(&dev));
+    if (!dn::lookup_batch_supported(query_embs, cache_embs, dim)) {
+      // other widths or alignments: one scan per query
+      void* ws = nullptr;
+      LookupRes* res = nullptr;
+      lookup_state(dev, &ws, &res);
+      for (int j = 0; j < nq; ++j) {
+        res->idx = -1;
+        res->score = 0.f;
+        dn::lookup(query_embs + (size_t)j * dim, cache_embs, n, dim, ws, &res->idx, &res->score, nullptr);
+        DN_HIP(hipStreamSynchronize(nullptr));
+        out_idx[j] = *static_cast<volatile long long*>(&res->idx);
+        if (out_score) out_score[j] = *static_cast<volatile float*>(&res->score);
+      }
+      return;
+    }
+    void* ws = nullptr;
+    long long* ridx = nullptr;
+    float* rscore = nullptr;
+    lookup_batch_state(dev, &ws, &ridx, &rscore);
+    const int mq = dn::lookup_batch_max_queries();
+    for (int j0 = 0; j0 < nq; j0 += mq) {
+      const int m = nq - j0 < mq ? nq - j0 : mq;
+      for (int j = 0; j < m; ++j) ridx[j] = -2;
+      dn::lookup_batch(query_embs + (size_t)j0 * dim, m, cache_embs, n, dim, ws, ridx, rscore, nullptr);
+      DN_HIP(hipStreamSynchronize(nullptr));
+      for (int j = 0; j < m; ++j) {
+        const long long idx = static_cast<volatile long long*>(ridx)[j];
+        DN_CHECK(idx >= -1 && idx < n, "ac_lookup_batch: result not written");
+        out_idx[j0 + j] = idx;
+        if (out_score) out_score[j0 + j] = static_cast<volatile float*>(rscore)[j];
+      }
+    }
   });
 }
 

@@ -170,5 +170,14 @@ void pack_bias(float* dst, int n, const float* src, int src_n, int row_mode, int
 size_t lookup_workspace_bytes();
 void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_out,
             float* score_out, hipStream_t s);
+// Top-1 rows of cache [n][dim] for nq <= lookup_batch_max_queries() queries q [nq][dim]
+// in one pass over the table (matrix-core scores). idx_out / score_out [nq] (device or
+// pinned host memory); idx -1 for a query with no defined cosine. Needs
+// lookup_batch_supported(q, cache, dim); ws: lookup_batch_workspace_bytes().
+size_t lookup_batch_workspace_bytes();
+int lookup_batch_max_queries();
+bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, int dim);
+void lookup_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n, int dim, void* ws,
+                  long long* idx_out, float* score_out, hipStream_t s);
 
 }  // namespace dn

@@ -7,6 +7,16 @@
 // (score, index); each workgroup writes the best of its 8 half-waves. Pass 2: one
 // workgroup reduces the per-workgroup winners. Ties go to the lowest index at every
 // stage, so the result is the first maximum, independent of the launch shape.
+//
+// Batched search (up to 64 queries per pass): the scores of a 16-row tile against all
+// queries are one [16 x dim] x [dim x 64] contraction on the matrix cores
+// (v_mfma_f32_16x16x32_f16: fp16 operands, exact products, fp32 sums), so the table is
+// read from HBM once per 64 queries instead of once per query. Each lane loads its
+// A operand (row l % 16, 8 consecutive dims at 8 * (l / 16)) straight from the table:
+// one 16-byte load per 32-dim k-step, 64 contiguous bytes per row per instruction.
+// The queries sit in LDS in B-fragment order (one conflict-free 16-byte read per lane
+// and k-step). Row norms come from the same A registers (packed fp16 dot products),
+// and the top-1 per query is kept in registers while the wave walks its tiles.
 #include "kernels.h"
 
 namespace dn {
@@ -218,6 +228,178 @@ __global__ __launch_bounds__(256) void reduce_kernel(const Cand* part, int nb, c
   }
 }
 
+
+// ---------------------------------------------------------------- batched search
+
+constexpr int kBatchQ = 64;          // queries per pass: 4 column tiles of 16
+constexpr int kBatchBlocks = 256;    // at most one workgroup per CU (the queries take up to 128 KB of LDS)
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// Waves per workgroup: the KS row registers of a tile (4 KS VGPRs) must leave room
+// for three waves per SIMD up to dim 768, two beyond.
+template <int KS> struct BatchWaves {
+  static constexpr int value = KS <= 24 ? 12 : 8;
+};
+
+// dim = 32 * KS. q [nq][dim] (nq <= 64), cache [n][dim]; part [gridDim.x][64] receives
+// each workgroup's best (score, index) per query (queries >= nq score zero and are ignored).
+template <int KS>
+__global__ __launch_bounds__(BatchWaves<KS>::value * 64) void scan_mfma_kernel(const uint16_t* q, int nq,
+                                                                             const uint16_t* cache, long long n,
+                                                                             Cand* part) {
+  constexpr int NW = BatchWaves<KS>::value;
+  constexpr int dim = 32 * KS;
+  extern __shared__ __align__(16) uint4 qf[];  // [4 column tiles][KS k-steps][64 lanes]
+  __shared__ Cand red[NW][kBatchQ];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int r16 = lane & 15, grp = lane >> 4;
+  for (int u = t; u < 4 * KS * 64; u += NW * 64) {
+    const int ln = u & 63, ks = (u >> 6) % KS, qt = (u >> 6) / KS;
+    const int qi = qt * 16 + (ln & 15);
+    qf[u] = qi < nq ? ld16(q + (long long)qi * dim + ks * 32 + 8 * (ln >> 4)) : make_uint4(0u, 0u, 0u, 0u);
+  }
+  __syncthreads();
+  float best_s[4];
+  long long best_i[4];
+#pragma unroll
+  for (int qt = 0; qt < 4; ++qt) {
+    best_s[qt] = -INFINITY;
+    best_i[qt] = n;
+  }
+  const long long tiles = (n + 15) / 16;
+  const long long stride = (long long)gridDim.x * NW;
+  for (long long tile = (long long)blockIdx.x * NW + w; tile < tiles; tile += stride) {
+    const long long row = tile * 16 + r16;
+    // past the end a lane re-reads the last row; its scores are not kept
+    const uint16_t* src = cache + (row < n ? row : n - 1) * dim + 8 * grp;
+    uint4 a[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) a[ks] = ld16(src + 32 * ks);
+    f32x4 acc[4];
+#pragma unroll
+    for (int qt = 0; qt < 4; ++qt) acc[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float cc = 0.f;
+    // opaque to the optimiser, so the query fragments are re-read from LDS per tile
+    // instead of being hoisted out of the loop into 16 KS registers
+    int ql = lane;
+    asm volatile("" : "+v"(ql));
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const f16x8 av = __builtin_bit_cast(f16x8, a[ks]);
+#pragma unroll
+      for (int qt = 0; qt < 4; ++qt)
+        acc[qt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(f16x8, qf[(qt * KS + ks) * 64 + ql]),
+                                                         acc[qt], 0, 0, 0);
+      const unsigned wd[4] = {a[ks].x, a[ks].y, a[ks].z, a[ks].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) cc = __builtin_amdgcn_fdot2(as_h2(wd[k]), as_h2(wd[k]), cc, false);
+    }
+    // |c|^2 of row r16: the four lane groups hold its four 8-dim slices of every k-step
+    cc += __shfl_xor(cc, 16, 64);
+    cc += __shfl_xor(cc, 32, 64);
+    // acc[qt][i] = c_(tile*16 + 4 grp + i) . q_(16 qt + r16)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = 4 * grp + i;
+      const float c2 = __shfl(cc, rr, 64);
+      const long long ri = tile * 16 + rr;
+      if (ri >= n) continue;
+#pragma unroll
+      for (int qt = 0; qt < 4; ++qt) {
+        const float sc = row_score(acc[qt][i], c2);
+        if (better(sc, ri, best_s[qt], best_i[qt])) {
+          best_s[qt] = sc;
+          best_i[qt] = ri;
+        }
+      }
+    }
+  }
+  // the four lane groups of a query column, then the waves in order
+#pragma unroll
+  for (int qt = 0; qt < 4; ++qt) {
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float s2 = __shfl_xor(best_s[qt], o, 64);
+      const long long i2 = __shfl_xor(best_i[qt], o, 64);
+      if (better(s2, i2, best_s[qt], best_i[qt])) {
+        best_s[qt] = s2;
+        best_i[qt] = i2;
+      }
+    }
+    if (grp == 0) red[w][qt * 16 + r16] = Cand{best_s[qt], best_i[qt]};
+  }
+  __syncthreads();
+  if (t < kBatchQ) {
+    Cand b = red[0][t];
+    for (int k = 1; k < NW; ++k)
+      if (better(red[k][t].s, red[k][t].i, b.s, b.i)) b = red[k][t];
+    part[(long long)blockIdx.x * kBatchQ + t] = b;
+  }
+}
+
+// One workgroup per query: the nb workgroup winners of its column, and |q|^2 for the
+// reported cosine. Writes idx[j] = -1 where the query has no defined cosine.
+__global__ __launch_bounds__(256) void reduce_batch_kernel(const Cand* part, int nb, const uint16_t* q, int dim,
+                                                           long long* idx, float* score) {
+  __shared__ float ws_s[4], ws_q[4];
+  __shared__ long long ws_i[4];
+  const int j = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  Cand c = t < nb ? part[(long long)t * kBatchQ + j] : Cand{-INFINITY, 0x7fffffffffffffffll};
+  float qq = 0.f;
+  for (int e = t; e < dim; e += 256) {
+    const float x = h2f(q[(long long)j * dim + e]);
+    qq += x * x;
+  }
+  float bs = c.s;
+  long long bi = c.i;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float s2 = __shfl_xor(bs, o, 64);
+    const long long i2 = __shfl_xor(bi, o, 64);
+    if (better(s2, i2, bs, bi)) {
+      bs = s2;
+      bi = i2;
+    }
+    qq += __shfl_xor(qq, o, 64);
+  }
+  if (lane == 0) {
+    ws_s[w] = bs;
+    ws_i[w] = bi;
+    ws_q[w] = qq;
+  }
+  __syncthreads();
+  if (t == 0) {
+    float qn = ws_q[0];
+    for (int k = 1; k < 4; ++k) {
+      if (better(ws_s[k], ws_i[k], bs, bi)) {
+        bs = ws_s[k];
+        bi = ws_i[k];
+      }
+      qn += ws_q[k];
+    }
+    idx[j] = (qn > 0.f && bs > -INFINITY) ? bi : -1;
+    score[j] = bs * rsqrtf(qn);
+  }
+}
+
+// Launches the scan over min(256, tiles / waves) workgroups; returns that count.
+template <int KS>
+int launch_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n, Cand* part, hipStream_t s) {
+  constexpr int NW = BatchWaves<KS>::value;
+  const long long want = ((n + 15) / 16 + NW - 1) / NW;
+  const int nb = static_cast<int>(want < kBatchBlocks ? want : kBatchBlocks);
+  const size_t lds = sizeof(uint4) * 4 * KS * 64;
+  static bool attr = false;  // per process: the attribute belongs to the code object
+  if (!attr) {
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&scan_mfma_kernel<KS>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+    attr = true;
+  }
+  hipLaunchKernelGGL(scan_mfma_kernel<KS>, dim3(nb), dim3(NW * 64), lds, s, q, nq, cache, n, part);
+  return nb;
+}
+
 }  // namespace
 
 size_t lookup_workspace_bytes() { return sizeof(Cand) * kScanBlocks; }
@@ -245,6 +427,36 @@ void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void
     hipLaunchKernelGGL(scan_scalar_kernel, dim3(nb), dim3(256), dim * sizeof(float), s, q, cache, n, dim, part);
   }
   hipLaunchKernelGGL(reduce_kernel, dim3(1), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out);
+  DN_HIP(hipGetLastError());
+}
+
+}  // namespace dn
+
+namespace dn {
+
+size_t lookup_batch_workspace_bytes() { return sizeof(Cand) * kBatchBlocks * kBatchQ; }
+
+int lookup_batch_max_queries() { return kBatchQ; }
+
+bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, int dim) {
+  const bool aligned = (reinterpret_cast<uintptr_t>(cache) % 16 == 0) && (reinterpret_cast<uintptr_t>(q) % 16 == 0);
+  return aligned && (dim == 256 || dim == 512 || dim == 768 || dim == 1024);
+}
+
+void lookup_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n, int dim, void* ws,
+                  long long* idx_out, float* score_out, hipStream_t s) {
+  DN_CHECK(n >= 1 && dim >= 1, "lookup_batch: empty cache");
+  DN_CHECK(nq >= 1 && nq <= kBatchQ, "lookup_batch: 1 to 64 queries per pass");
+  DN_CHECK(lookup_batch_supported(q, cache, dim), "lookup_batch: dim must be 256, 512, 768 or 1024, 16-byte aligned");
+  Cand* part = static_cast<Cand*>(ws);
+  int nb = 0;
+  switch (dim) {
+    case 256: nb = launch_batch<8>(q, nq, cache, n, part, s); break;
+    case 512: nb = launch_batch<16>(q, nq, cache, n, part, s); break;
+    case 768: nb = launch_batch<24>(q, nq, cache, n, part, s); break;
+    default: nb = launch_batch<32>(q, nq, cache, n, part, s); break;
+  }
+  hipLaunchKernelGGL(reduce_batch_kernel, dim3(nq), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out);
   DN_HIP(hipGetLastError());
 }
 

@@ -22,7 +22,7 @@ ABI_VERSION = 1
 MAX_LEVELS = 4
 
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_unet_eps", "ac_lookup",
-            "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
+            "ac_lookup_batch", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
             "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_linear_vt", "dn_destroy",
             "dn_last_error")
 
@@ -67,6 +67,7 @@ def _load():
         "dn_denoise": [P, P, P, P, I32, I32, I32, F32, P],
         "dn_unet_eps": [P, P, I32, P, F32, P, P, P],
         "ac_lookup": [P, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
+        "ac_lookup_batch": [P, I32, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
         "ac_fetch_latent": [P, I64, I64, I64, P, P],
         "dn_packed_weight_elems": [I32, I32, I32, C.POINTER(I64)],
         "dn_pack_weight": [I32, P, I32, I32, P, P],
@@ -202,6 +203,19 @@ def ac_lookup_raw(query_ptr, cache_ptr, n, dim):
     score = C.c_float()
     code = lib.ac_lookup(query_ptr, cache_ptr, n, dim, C.byref(idx), C.byref(score))
     return code, idx.value, score.value
+
+
+def ac_lookup_batch(queries, cache):
+    """(indices, cosines) of the nearest cache row for every query: queries [nq, dim],
+    cache [n, dim] fp16 CUDA tensors. Lists of length nq; index -1 for a zero query."""
+    nq, dim = queries.shape
+    n = cache.shape[0]
+    if cache.shape[1] != dim:
+        raise ValueError("ac_lookup_batch: query and cache widths differ")
+    idx = (C.c_int64 * nq)()
+    score = (C.c_float * nq)()
+    _check(lib.ac_lookup_batch(_ptr(queries), nq, _ptr(cache), n, dim, idx, score))
+    return list(idx), list(score)
 
 
 def ac_fetch_latent(cache_latents, idx, latent, stream=None):

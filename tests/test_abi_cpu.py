@@ -86,6 +86,12 @@ def test_null_and_range_errors_touch_nothing():
     for q, cache, n, dim in [(None, 1, 5, 8), (1, None, 5, 8), (1, 1, 0, 8), (1, 1, 5, 0), (1, 1, -3, 8)]:
         code, idx, _ = dn.ac_lookup_raw(q, cache, n, dim)
         assert code == dn.DN_EINVAL and idx == -7
+    # batched lookup: null pointers, nq / n / dim <= 0 -> DN_EINVAL, outputs untouched
+    out = (C.c_int64 * 2)(-7, -7)
+    for q, nq, cache, n, dim in [(None, 2, 1, 5, 8), (1, 2, None, 5, 8), (1, 0, 1, 5, 8), (1, 2, 1, 0, 8),
+                                 (1, 2, 1, 5, 0), (1, -1, 1, 5, 8)]:
+        assert dn.lib.ac_lookup_batch(q, nq, cache, n, dim, out, None) == dn.DN_EINVAL
+        assert list(out) == [-7, -7]
     # denoise / unet hooks with a null handle
     assert dn.lib.dn_denoise(None, None, None, None, 0, 0, 0, 7.5, None) == dn.DN_EINVAL
     assert dn.lib.dn_unet_eps(None, None, 0, None, 7.5, None, None, None) == dn.DN_EINVAL

@@ -69,3 +69,87 @@ def test_zero_query_is_an_error_and_fetch_is_exact():
     dn.ac_fetch_latent(lat, 6, out)
     torch.cuda.synchronize()
     assert torch.equal(out, lat[6].float())
+
+
+# ----------------------------------------------------------------------------- batched search
+
+def _dev16(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.uint16)).to(DEV)
+
+
+def _check_batch(qs, cache, idx, score):
+    """Index bit-exact unless the oracle's scores of the two rows differ by < 1e-6;
+    cosine within 1e-5; -1 exactly where the oracle has no defined cosine."""
+    ridx, rsc = OL.top1_batch(qs, cache)
+    s = OL.cosine_scores_batch(qs, cache)
+    for j in range(len(ridx)):
+        if ridx[j] < 0:
+            assert idx[j] == -1, (j, idx[j])
+            continue
+        assert 0 <= idx[j] < cache.shape[0]
+        if idx[j] != ridx[j]:
+            assert abs(s[j, idx[j]] - s[j, ridx[j]]) < 1e-6, (j, idx[j], ridx[j])
+        assert abs(score[j] - rsc[j]) < 1e-5, (j, score[j], rsc[j])
+    return ridx
+
+
+def test_batch_planted_full_cache():
+    announce("lookup batch: 100000 x 768, 64 planted queries")
+    cache = W.cache_embeddings(100_000, 768, seed=7)
+    qs, rows = W.planted_queries(cache, 64, seed=11)
+    qs = np.stack(qs)
+    idx, score = dn.ac_lookup_batch(_dev16(qs), _dev16(cache))
+    _check_batch(qs, cache, idx, score)
+    assert list(idx) == list(rows)
+
+
+@pytest.mark.parametrize("nq,n,dim", [(1, 1, 768), (5, 17, 256), (64, 1001, 512), (70, 4097, 768),
+                                      (3, 300, 1024), (2, 15, 768), (7, 200, 77), (9, 33, 1536)])
+def test_batch_ragged_sizes_zero_rows_and_queries(nq, n, dim):
+    announce(f"lookup batch: nq={nq} n={n} dim={dim}")
+    rng = np.random.default_rng(nq * 1000 + n + dim)
+    cache = rng.standard_normal((n, dim)).astype(np.float16)
+    qs = rng.standard_normal((nq, dim)).astype(np.float16)
+    if n > 3:
+        cache[n // 2] = 0
+        qs[0] = cache[n // 2 + 1]
+    if nq > 2:
+        qs[nq - 2] = 0
+    idx, score = dn.ac_lookup_batch(_dev16(qs), _dev16(cache))
+    ridx = _check_batch(qs, cache, idx, score)
+    if nq > 2:
+        assert idx[nq - 2] == -1 and ridx[nq - 2] == -1
+    if n > 3:
+        assert idx[0] == n // 2 + 1
+
+
+def test_batch_agrees_with_single_query_search():
+    announce("lookup batch vs ac_lookup: 20000 x 768")
+    cache = W.cache_embeddings(20_000, 768, seed=5)
+    rng = np.random.default_rng(2)
+    qs = rng.standard_normal((16, 768)).astype(np.float16)
+    cd = _dev16(cache)
+    idx, score = dn.ac_lookup_batch(_dev16(qs), cd)
+    s = OL.cosine_scores_batch(qs, cache)
+    for j in range(16):
+        i1, s1 = dn.ac_lookup(_dev16(qs[j]), cd)
+        if i1 != idx[j]:
+            assert abs(s[j, i1] - s[j, idx[j]]) < 1e-6
+        assert abs(s1 - score[j]) < 2e-6
+
+
+def test_batch_duplicates_give_lowest_index_and_errors_touch_nothing():
+    announce("lookup batch: duplicates, argument errors")
+    cache = W.cache_embeddings(20_000, 768, seed=3)
+    for j in (17, 9999, 19_999):
+        cache[j - 10] = cache[j]
+    cache[12_345] = cache[17]
+    qs = np.stack([cache[17], cache[9999], cache[19_999], cache[12_345]])
+    idx, score = dn.ac_lookup_batch(_dev16(qs), _dev16(cache))
+    assert list(idx) == [7, 9989, 19_989, 7]
+    assert all(abs(v - 1.0) < 1e-6 for v in score)
+    import ctypes as C
+    out = (C.c_int64 * 2)(-7, -7)
+    assert dn.lib.ac_lookup_batch(None, 2, 1, 5, 768, out, None) == dn.DN_EINVAL
+    assert dn.lib.ac_lookup_batch(1, 0, 1, 5, 768, out, None) == dn.DN_EINVAL
+    assert list(out) == [-7, -7]

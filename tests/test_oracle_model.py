@@ -319,3 +319,34 @@ def test_lookup_planted_and_ties():
     dup[4000] = dup[123]
     assert lookup.top1(dup[123], dup)[0] == 123
     assert lookup.top2_gap(dup[123], dup) == 0.0
+
+
+def test_lookup_batch_against_brute_force_and_invariants():
+    rng = np.random.default_rng(21)
+    cache = rng.standard_normal((29, 7)).astype(np.float16)
+    cache[5] = 0  # zero row: never selected
+    qs = rng.standard_normal((6, 7)).astype(np.float16)
+    qs[2] = 0  # zero query: no defined cosine
+    qs[4] = cache[11] * np.float16(4)  # exact positive multiple of a row: cosine 1 with it
+    idx, sc = lookup.top1_batch(qs, cache)
+    for j, q in enumerate(qs):
+        qq = [float(v) for v in q]
+        nq = math.sqrt(sum(b * b for b in qq))
+        if nq == 0:
+            assert idx[j] == -1 and math.isnan(sc[j])
+            continue
+        best, best_s = -1, -math.inf
+        for i in range(cache.shape[0]):
+            c = [float(v) for v in cache[i]]
+            nc = math.sqrt(sum(a * a for a in c))
+            if nc == 0:
+                continue
+            s = sum(a * b for a, b in zip(c, qq)) / nc / nq
+            if s > best_s:
+                best, best_s = i, s
+        assert idx[j] == best and abs(sc[j] - best_s) < 1e-12
+    assert idx[4] == 11 and abs(sc[4] - 1.0) < 1e-12
+    # permuting the queries permutes the answers
+    perm = rng.permutation(6)
+    idx2, _ = lookup.top1_batch(qs[perm], cache)
+    assert np.array_equal(idx2, idx[perm])
