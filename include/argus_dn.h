@@ -202,7 +202,7 @@ dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64
  * over cache_embs (device fp16 [n][dim]): out_idx[j] (host int64 [nq]) receives
  * the first row of maximal cosine with query j, or -1 when query j is zero (or
  * every row is), and out_score[j] (host float [nq], may be NULL) that cosine.
- * For dim 256, 512, 768 or 1024 with 16-byte aligned pointers the table is read
+ * For dim 256, 512, 768 or 1024, 16-byte aligned pointers and n < 2^31 - 64, the table is read
  * once per 64 queries and the scores are matrix-core products (fp16 operands,
  * fp32 sums); other widths run one ac_lookup scan per query. Synchronous (default
  * stream). nq >= 1, n >= 1, dim >= 1; on an argument error nothing is written.

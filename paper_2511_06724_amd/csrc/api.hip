@@ -224,7 +224,7 @@ dn_status ac_lookup_batch(const uint16_t* query_embs, int32_t nq, const uint16_t
     DN_CHECK(dim >= 1, "ac_lookup_batch: dim must be >= 1");
     int dev = 0;
     DN_HIP(hipGetDevice(&dev));
-    if (!dn::lookup_batch_supported(query_embs, cache_embs, dim)) {
+    if (!dn::lookup_batch_supported(query_embs, cache_embs, n, dim)) {
       // other widths or alignments: one scan per query
       void* ws = nullptr;
       LookupRes* res = nullptr;

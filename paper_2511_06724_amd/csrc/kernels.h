@@ -176,7 +176,7 @@ void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void
 // lookup_batch_supported(q, cache, dim); ws: lookup_batch_workspace_bytes().
 size_t lookup_batch_workspace_bytes();
 int lookup_batch_max_queries();
-bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, int dim);
+bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, long long n, int dim);
 void lookup_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n, int dim, void* ws,
                   long long* idx_out, float* score_out, hipStream_t s);
 

@@ -236,19 +236,21 @@ constexpr int kBatchBlocks = 256;    // at most one workgroup per CU (the querie
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
-// Waves per workgroup: the KS row registers of a tile (4 KS VGPRs) must leave room
-// for three waves per SIMD up to dim 768, two beyond.
-template <int KS> struct BatchWaves {
-  static constexpr int value = KS <= 24 ? 12 : 8;
+// Two register sets of a tile's rows (4 KS VGPRs each) when they fit beside three
+// (KS = 8) or two waves per SIMD: the next tile's loads are then in flight while the
+// current tile is scored. dim 1024 keeps one set (two waves per SIMD).
+template <int KS> struct BatchCfg {
+  static constexpr bool kTwoSets = KS <= 24;
+  static constexpr int kWaves = KS <= 8 ? 12 : 8;
 };
 
 // dim = 32 * KS. q [nq][dim] (nq <= 64), cache [n][dim]; part [gridDim.x][64] receives
 // each workgroup's best (score, index) per query (queries >= nq score zero and are ignored).
 template <int KS>
-__global__ __launch_bounds__(BatchWaves<KS>::value * 64) void scan_mfma_kernel(const uint16_t* q, int nq,
-                                                                             const uint16_t* cache, long long n,
-                                                                             Cand* part) {
-  constexpr int NW = BatchWaves<KS>::value;
+__global__ __launch_bounds__(BatchCfg<KS>::kWaves * 64) void scan_mfma_kernel(const uint16_t* q, int nq,
+                                                                            const uint16_t* cache, int n,
+                                                                            Cand* part) {
+  constexpr int NW = BatchCfg<KS>::kWaves;
   constexpr int dim = 32 * KS;
   extern __shared__ __align__(16) uint4 qf[];  // [4 column tiles][KS k-steps][64 lanes]
   __shared__ Cand red[NW][kBatchQ];
@@ -261,21 +263,23 @@ __global__ __launch_bounds__(BatchWaves<KS>::value * 64) void scan_mfma_kernel(c
   }
   __syncthreads();
   float best_s[4];
-  long long best_i[4];
+  int best_i[4];
 #pragma unroll
   for (int qt = 0; qt < 4; ++qt) {
     best_s[qt] = -INFINITY;
     best_i[qt] = n;
   }
-  const long long tiles = (n + 15) / 16;
-  const long long stride = (long long)gridDim.x * NW;
-  for (long long tile = (long long)blockIdx.x * NW + w; tile < tiles; tile += stride) {
-    const long long row = tile * 16 + r16;
-    // past the end a lane re-reads the last row; its scores are not kept
-    const uint16_t* src = cache + (row < n ? row : n - 1) * dim + 8 * grp;
-    uint4 a[KS];
+  const int tiles = (n + 15) / 16;
+  const int stride = gridDim.x * NW;
+
+  // the lane's 16-byte slices of row tile * 16 + r16 (past the end: the last row, not scored)
+  auto load = [&](uint4 (&a)[KS], int tile) {
+    const int row = tile * 16 + r16;
+    const uint16_t* src = cache + (long long)(row < n ? row : n - 1) * dim + 8 * grp;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) a[ks] = ld16(src + 32 * ks);
+  };
+  auto score = [&](const uint4 (&a)[KS], int tile) {
     f32x4 acc[4];
 #pragma unroll
     for (int qt = 0; qt < 4; ++qt) acc[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -303,7 +307,7 @@ __global__ __launch_bounds__(BatchWaves<KS>::value * 64) void scan_mfma_kernel(c
     for (int i = 0; i < 4; ++i) {
       const int rr = 4 * grp + i;
       const float c2 = __shfl(cc, rr, 64);
-      const long long ri = tile * 16 + rr;
+      const int ri = tile * 16 + rr;
       if (ri >= n) continue;
 #pragma unroll
       for (int qt = 0; qt < 4; ++qt) {
@@ -314,6 +318,26 @@ __global__ __launch_bounds__(BatchWaves<KS>::value * 64) void scan_mfma_kernel(c
         }
       }
     }
+  };
+
+  const int first = blockIdx.x * NW + w;
+  if constexpr (BatchCfg<KS>::kTwoSets) {
+    uint4 a0[KS], a1[KS];
+    if (first < tiles) load(a0, first);
+    for (int tile = first; tile < tiles; tile += 2 * stride) {
+      const int t1 = tile + stride;
+      if (t1 < tiles) load(a1, t1);
+      score(a0, tile);
+      if (t1 >= tiles) break;
+      if (t1 + stride < tiles) load(a0, t1 + stride);
+      score(a1, t1);
+    }
+  } else {
+    uint4 a0[KS];
+    for (int tile = first; tile < tiles; tile += stride) {
+      load(a0, tile);
+      score(a0, tile);
+    }
   }
   // the four lane groups of a query column, then the waves in order
 #pragma unroll
@@ -321,7 +345,7 @@ __global__ __launch_bounds__(BatchWaves<KS>::value * 64) void scan_mfma_kernel(c
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
       const float s2 = __shfl_xor(best_s[qt], o, 64);
-      const long long i2 = __shfl_xor(best_i[qt], o, 64);
+      const int i2 = __shfl_xor(best_i[qt], o, 64);
       if (better(s2, i2, best_s[qt], best_i[qt])) {
         best_s[qt] = s2;
         best_i[qt] = i2;
@@ -385,8 +409,8 @@ __global__ __launch_bounds__(256) void reduce_batch_kernel(const Cand* part, int
 
 // Launches the scan over min(256, tiles / waves) workgroups; returns that count.
 template <int KS>
-int launch_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n, Cand* part, hipStream_t s) {
-  constexpr int NW = BatchWaves<KS>::value;
+int launch_batch(const uint16_t* q, int nq, const uint16_t* cache, int n, Cand* part, hipStream_t s) {
+  constexpr int NW = BatchCfg<KS>::kWaves;
   const long long want = ((n + 15) / 16 + NW - 1) / NW;
   const int nb = static_cast<int>(want < kBatchBlocks ? want : kBatchBlocks);
   const size_t lds = sizeof(uint4) * 4 * KS * 64;
@@ -438,7 +462,8 @@ size_t lookup_batch_workspace_bytes() { return sizeof(Cand) * kBatchBlocks * kBa
 
 int lookup_batch_max_queries() { return kBatchQ; }
 
-bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, int dim) {
+bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, long long n, int dim) {
+  if (n > (1ll << 31) - 64) return false;  // 32-bit row indices in the scan
   const bool aligned = (reinterpret_cast<uintptr_t>(cache) % 16 == 0) && (reinterpret_cast<uintptr_t>(q) % 16 == 0);
   return aligned && (dim == 256 || dim == 512 || dim == 768 || dim == 1024);
 }
@@ -447,14 +472,16 @@ void lookup_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n,
                   long long* idx_out, float* score_out, hipStream_t s) {
   DN_CHECK(n >= 1 && dim >= 1, "lookup_batch: empty cache");
   DN_CHECK(nq >= 1 && nq <= kBatchQ, "lookup_batch: 1 to 64 queries per pass");
-  DN_CHECK(lookup_batch_supported(q, cache, dim), "lookup_batch: dim must be 256, 512, 768 or 1024, 16-byte aligned");
+  DN_CHECK(lookup_batch_supported(q, cache, n, dim),
+           "lookup_batch: dim must be 256, 512, 768 or 1024, 16-byte aligned, n < 2^31 - 64");
+  const int n32 = static_cast<int>(n);
   Cand* part = static_cast<Cand*>(ws);
   int nb = 0;
   switch (dim) {
-    case 256: nb = launch_batch<8>(q, nq, cache, n, part, s); break;
-    case 512: nb = launch_batch<16>(q, nq, cache, n, part, s); break;
-    case 768: nb = launch_batch<24>(q, nq, cache, n, part, s); break;
-    default: nb = launch_batch<32>(q, nq, cache, n, part, s); break;
+    case 256: nb = launch_batch<8>(q, nq, cache, n32, part, s); break;
+    case 512: nb = launch_batch<16>(q, nq, cache, n32, part, s); break;
+    case 768: nb = launch_batch<24>(q, nq, cache, n32, part, s); break;
+    default: nb = launch_batch<32>(q, nq, cache, n32, part, s); break;
   }
   hipLaunchKernelGGL(reduce_batch_kernel, dim3(nq), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out);
   DN_HIP(hipGetLastError());

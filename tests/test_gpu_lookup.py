@@ -104,7 +104,8 @@ def test_batch_planted_full_cache():
 
 
 @pytest.mark.parametrize("nq,n,dim", [(1, 1, 768), (5, 17, 256), (64, 1001, 512), (70, 4097, 768),
-                                      (3, 300, 1024), (2, 15, 768), (7, 200, 77), (9, 33, 1536)])
+                                      (3, 300, 1024), (2, 15, 768), (7, 200, 77), (9, 33, 1536),
+                                      (8, 60001, 256), (4, 40003, 512), (5, 70001, 1024)])
 def test_batch_ragged_sizes_zero_rows_and_queries(nq, n, dim):
     announce(f"lookup batch: nq={nq} n={n} dim={dim}")
     rng = np.random.default_rng(nq * 1000 + n + dim)
