@@ -13,6 +13,7 @@
  *   dn_weight_count / dn_weight_table  size and describe the canonical weight blob
  *   dn_create                          build a denoiser (pack weights for the GPU)
  *   dn_denoise                         run iterations [start_step, start_step + n_steps)
+ *   dn_denoise_capture                 the same, writing the latent after chosen iterations (cache write)
  *   ac_lookup                          top-1 cosine search over the prompt-embedding cache
  *   ac_lookup_batch                    the same search for many queries in one pass over the cache
  *   ac_fetch_latent                    copy cached latent #idx into an fp32 latent buffer
@@ -174,6 +175,23 @@ dn_status dn_create(const dn_config* cfg, const float* weights, size_t n_floats,
  * stream at a time (its workspace is reused by every call). */
 dn_status dn_denoise(dn_handle* h, float* latent, const float* text_ctx, const int32_t* timesteps,
                      int32_t n_timesteps, int32_t start_step, int32_t n_steps, float cfg_scale, void* stream);
+
+/* Denoise loop that also writes the cache (Sec. 4.7: every prompt stores its
+ * intermediate states at K, which later prompts resume from, Sec. 2.1): runs
+ * exactly dn_denoise(h, latent, text_ctx, timesteps, n_timesteps, start_step,
+ * n_steps, cfg_scale, stream) and, for each j < n_capture, writes the latent
+ * after capture_at[j] iterations, i.e. x at timesteps[capture_at[j]], rounded to
+ * bf16 (nearest, ties to even), to out_latents + j * B*latent_c*H*W.
+ * capture_at   host int32 [n_capture], each in [start_step, start_step + n_steps]
+ *              (start_step captures the input latent); read during the call only.
+ * out_latents  device bf16 [n_capture][B][latent_c][H][W], the layout of the cache's
+ *              latent table (a slot is what ac_fetch_latent reads back).
+ * n_capture = 0 is dn_denoise. Capture arguments are checked with the others,
+ * before anything is enqueued. Asynchronous on `stream`; the result latent and
+ * the final state are bitwise those of dn_denoise. */
+dn_status dn_denoise_capture(dn_handle* h, float* latent, const float* text_ctx, const int32_t* timesteps,
+                             int32_t n_timesteps, int32_t start_step, int32_t n_steps, float cfg_scale,
+                             const int32_t* capture_at, int32_t n_capture, uint16_t* out_latents, void* stream);
 
 /* One UNet evaluation + guidance at timestep t (no DDIM update), for checking a
  * single iteration. x device fp32 [B][latent_c][H][W]; text_ctx as in dn_denoise;

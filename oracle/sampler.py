@@ -48,3 +48,25 @@ def denoise(cfg, W, x, ctx, timesteps, start_step, n_steps, cfg_scale, trace=Non
         if trace is not None:
             trace.append(x.copy())
     return x
+
+
+def bf16_round(x):
+    """fp32 -> bf16 -> fp32 with round-to-nearest, ties to even: keep the upper 16
+    bits of the IEEE single after adding half a unit of the kept part (0x7fff) plus
+    the kept part's lowest bit (which breaks a tie towards the even neighbour).
+    Finite inputs only."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+    return b.astype(np.uint32).view(np.float32)
+
+
+def denoise_capture(cfg, W, x, ctx, timesteps, start_step, n_steps, cfg_scale, capture_at):
+    """The cache write of Sec. 4.7 (a prompt's run stores its intermediate states at
+    K): runs `denoise` and returns (final latent, [bf16_round(latent after K
+    iterations) for K in capture_at]); K = start_step is the input latent."""
+    for k in capture_at:
+        if not start_step <= k <= start_step + n_steps:
+            raise ValueError("capture iteration outside [start_step, start_step + n_steps]")
+    trace = [np.asarray(x, dtype=np.float32).copy()]
+    final = denoise(cfg, W, x, ctx, timesteps, start_step, n_steps, cfg_scale, trace=trace)
+    return final, [bf16_round(trace[k - start_step]) for k in capture_at]

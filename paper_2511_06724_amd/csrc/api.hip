@@ -183,6 +183,16 @@ dn_status dn_denoise(dn_handle* h, float* latent, const float* text_ctx, const i
   });
 }
 
+dn_status dn_denoise_capture(dn_handle* h, float* latent, const float* text_ctx, const int32_t* timesteps,
+                             int32_t n_timesteps, int32_t start_step, int32_t n_steps, float cfg_scale,
+                             const int32_t* capture_at, int32_t n_capture, uint16_t* out_latents, void* stream) {
+  return guarded([&] {
+    DN_CHECK(h && h->m, "dn_denoise_capture: null handle");
+    dn::model_denoise(h->m, latent, text_ctx, timesteps, n_timesteps, start_step, n_steps, cfg_scale,
+                      as_stream(stream), capture_at, n_capture, out_latents);
+  });
+}
+
 dn_status dn_unet_eps(dn_handle* h, const float* x, int32_t t, const float* text_ctx, float cfg_scale, float* out_raw,
                       float* out_guided, void* stream) {
   return guarded([&] {

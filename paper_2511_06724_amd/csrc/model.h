@@ -32,7 +32,8 @@ struct Model;
 Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats, bool on_device);
 void model_destroy(Model* m);
 void model_denoise(Model* m, float* latent, const float* ctx, const int32_t* ts, int n_ts, int start, int n,
-                   float scale, hipStream_t s);
+                   float scale, hipStream_t s, const int32_t* cap_at = nullptr, int n_cap = 0,
+                   uint16_t* cap_out = nullptr);
 void model_unet_eps(Model* m, const float* x, int t, const float* ctx, float scale, float* raw, float* guided,
                     hipStream_t s);
 

@@ -1133,19 +1133,30 @@ void time_features(Model* m, const int32_t* ts, int n, hipStream_t s) {
   }
 }
 
+// Writes the latent, rounded to bf16, to every capture slot j whose iteration count
+// cap_at[j] equals `done` (the cache stores a prompt's state after K iterations).
+void capture_latent(const float* latent, long long numel, int done, const int32_t* cap_at, int n_cap, uint16_t* out,
+                    hipStream_t s) {
+  for (int j = 0; j < n_cap; ++j)
+    if (cap_at[j] == done) convert_from_f32<bf16>(latent, reinterpret_cast<bf16*>(out) + j * numel, numel, s);
+}
+
 template <typename T>
 void denoise_t(Model* m, float* latent, const float* ctx, const int32_t* ts, int start, int n_steps, float scale,
-               hipStream_t s) {
+               const int32_t* cap_at, int n_cap, uint16_t* cap_out, hipStream_t s) {
   const dn_config& c = m->cfg;
   Exec<T> ex{m, s, m->n};
   time_features(m, ts + start, n_steps, s);
   ex.prepare(ctx, n_steps);
   const int HW = c.latent_h * c.latent_w;
+  const long long numel = (long long)c.batch * c.latent_c * HW;
+  capture_latent(latent, numel, start, cap_at, n_cap, cap_out, s);
   latent_to_input<T>(latent, static_cast<T*>(m->xin), c.batch, c.latent_c, HW, kCinPad, s);
   for (int i = 0; i < n_steps; ++i) {
     ex.unet(i);
     cfg_ddim<T>(m->eps, latent, static_cast<T*>(m->xin), m->abar, ts[start + i], ts[start + i + 1], scale, c.batch,
                 c.latent_c, HW, kCinPad, s);
+    capture_latent(latent, numel, start + i + 1, cap_at, n_cap, cap_out, s);
   }
 }
 
@@ -1165,18 +1176,28 @@ void unet_eps_t(Model* m, const float* x, int t, const float* ctx, float scale, 
 }  // namespace
 
 void model_denoise(Model* m, float* latent, const float* ctx, const int32_t* ts, int n_ts, int start, int n,
-                   float scale, hipStream_t s) {
+                   float scale, hipStream_t s, const int32_t* cap_at, int n_cap, uint16_t* cap_out) {
   DN_CHECK(latent && ctx && ts, "dn_denoise: null pointer");
+  DN_CHECK(n_cap >= 0, "dn_denoise_capture: n_capture must be >= 0");
+  DN_CHECK(n_cap == 0 || (cap_at && cap_out), "dn_denoise_capture: null capture pointer");
+  for (int j = 0; j < n_cap; ++j)
+    DN_CHECK(cap_at[j] >= start && (int64_t)cap_at[j] <= (int64_t)start + n,
+             "dn_denoise_capture: capture iteration outside [start_step, start_step + n_steps]");
   DN_CHECK(start >= 0 && n >= 0, "dn_denoise: start_step and n_steps must be >= 0");
   DN_CHECK((int64_t)start + n + 1 <= n_ts, "dn_denoise: timesteps shorter than start_step + n_steps + 1");
   DN_CHECK(n <= kMaxSteps, "dn_denoise: n_steps > 1000");
   for (int i = start; i <= start + n; ++i)
     DN_CHECK(ts[i] >= -1 && ts[i] < m->cfg.n_train_steps, "dn_denoise: timestep out of range");
-  if (n == 0) return;
+  if (n == 0) {
+    // nothing to run; a capture at start_step is still the input latent
+    capture_latent(latent, (long long)m->cfg.batch * m->cfg.latent_c * m->cfg.latent_h * m->cfg.latent_w, start,
+                   cap_at, n_cap, cap_out, s);
+    return;
+  }
   if (m->bf)
-    denoise_t<bf16>(m, latent, ctx, ts, start, n, scale, s);
+    denoise_t<bf16>(m, latent, ctx, ts, start, n, scale, cap_at, n_cap, cap_out, s);
   else
-    denoise_t<float>(m, latent, ctx, ts, start, n, scale, s);
+    denoise_t<float>(m, latent, ctx, ts, start, n, scale, cap_at, n_cap, cap_out, s);
 }
 
 void model_unet_eps(Model* m, const float* x, int t, const float* ctx, float scale, float* raw, float* guided,

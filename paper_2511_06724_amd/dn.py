@@ -21,7 +21,7 @@ DN_WEIGHTS_HOST, DN_WEIGHTS_DEVICE = 0, 1
 ABI_VERSION = 1
 MAX_LEVELS = 4
 
-EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_unet_eps", "ac_lookup",
+EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_denoise_capture", "dn_unet_eps", "ac_lookup",
             "ac_lookup_batch", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
             "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_linear_vt", "dn_destroy",
             "dn_last_error")
@@ -65,6 +65,7 @@ def _load():
         "dn_weight_table": [C.POINTER(_Config), P, P, P, SZ, C.POINTER(SZ)],
         "dn_create": [C.POINTER(_Config), P, SZ, I32, C.POINTER(P)],
         "dn_denoise": [P, P, P, P, I32, I32, I32, F32, P],
+        "dn_denoise_capture": [P, P, P, P, I32, I32, I32, F32, P, I32, P, P],
         "dn_unet_eps": [P, P, I32, P, F32, P, P, P],
         "ac_lookup": [P, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
         "ac_lookup_batch": [P, I32, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
@@ -183,6 +184,16 @@ class Denoiser:
         ts = np.ascontiguousarray(timesteps, dtype=np.int32)
         _check(lib.dn_denoise(self._h, _ptr(latent), _ptr(text_ctx), ts.ctypes.data, ts.size, start_step, n_steps,
                               cfg_scale, _stream(stream)))
+
+    def denoise_capture(self, latent, text_ctx, timesteps, start_step, n_steps, cfg_scale, capture_at, out_latents,
+                        stream=None):
+        """dn_denoise that also writes the latent after each iteration count in capture_at
+        (bf16) to out_latents [len(capture_at), B, C, H, W] (a bf16 CUDA tensor)."""
+        ts = np.ascontiguousarray(timesteps, dtype=np.int32)
+        cap = np.ascontiguousarray(capture_at, dtype=np.int32)
+        _check(lib.dn_denoise_capture(self._h, _ptr(latent), _ptr(text_ctx), ts.ctypes.data, ts.size, start_step,
+                                      n_steps, cfg_scale, cap.ctypes.data if cap.size else None, cap.size,
+                                      _ptr(out_latents), _stream(stream)))
 
     def unet_eps(self, x, t, text_ctx, cfg_scale, out_raw, out_guided=None, stream=None):
         _check(lib.dn_unet_eps(self._h, _ptr(x), int(t), _ptr(text_ctx), cfg_scale, _ptr(out_raw),

@@ -95,6 +95,7 @@ def test_null_and_range_errors_touch_nothing():
     # denoise / unet hooks with a null handle
     assert dn.lib.dn_denoise(None, None, None, None, 0, 0, 0, 7.5, None) == dn.DN_EINVAL
     assert dn.lib.dn_unet_eps(None, None, 0, None, 7.5, None, None, None) == dn.DN_EINVAL
+    assert dn.lib.dn_denoise_capture(None, None, None, None, 0, 0, 0, 7.5, None, 0, None, None) == dn.DN_EINVAL
     # create: blob length mismatch is rejected before any device work
     blob = np.zeros(10, np.float32)
     h = C.c_void_p()

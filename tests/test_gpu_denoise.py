@@ -182,3 +182,65 @@ def test_sdxl_step_properties():
     assert torch.isfinite(a).all()
     assert torch.equal(a, b)
     model.close()
+
+
+# ----------------------------------------------------------------------------- cache write
+
+def _bf16_bits(t):
+    return t.contiguous().view(torch.int16).cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", [W.DN_FP32, W.DN_BF16])
+def test_capture_is_the_run_rounded_to_bf16(dtype):
+    """dn_denoise_capture leaves the run bitwise unchanged; each slot is bitwise the
+    bf16 rounding of the latent after K iterations of the same library; against the
+    oracle's captured trajectory within the trajectory bar."""
+    announce(f"capture dtype={dtype}")
+    cfg = W.tiny(dtype)
+    model, Wt = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    cd = f32_dev(ctx)
+    ts = S.default_timesteps(10)
+    start, n, caps = 1, 9, [1, 3, 5, 10, 3]
+    plain = f32_dev(x)
+    model.denoise(plain, cd, ts, start, n, 7.5)
+    lat = f32_dev(x)
+    out = torch.full((len(caps), cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), float("nan"), device=DEV,
+                     dtype=torch.bfloat16)
+    model.denoise_capture(lat, cd, ts, start, n, 7.5, caps, out)
+    torch.cuda.synchronize()
+    assert torch.equal(lat, plain)
+    for j, k in enumerate(caps):
+        mid = f32_dev(x)
+        model.denoise(mid, cd, ts, start, k - start, 7.5)
+        torch.cuda.synchronize()
+        assert np.array_equal(_bf16_bits(out[j]), _bf16_bits(mid.to(torch.bfloat16))), k
+    ref_final, ref_caps = sampler.denoise_capture(cfg, Wt, x, ctx, ts, start, n, 7.5, caps)
+    bar = 2e-3 if dtype == W.DN_FP32 else 5e-2
+    for j, k in enumerate(caps):
+        e = rel_l2(out[j].float().cpu().numpy(), ref_caps[j])
+        announce(f"  K={k} rel-L2 {e:.3e}")
+        assert e <= bar, (k, e)
+
+
+def test_capture_argument_errors_enqueue_nothing():
+    announce("capture argument errors")
+    cfg = W.tiny(W.DN_FP32)
+    model, _ = _model(cfg)
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    ts = S.default_timesteps(10)
+    lat = f32_dev(x)
+    before = lat.clone()
+    out = torch.zeros((1, cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device=DEV, dtype=torch.bfloat16)
+    for caps in ([0], [7], [2, 7]):  # outside [start_step, start_step + n_steps] = [1, 6]
+        with pytest.raises(dn.DnError):
+            model.denoise_capture(lat, f32_dev(ctx), ts, 1, 5, 7.5, caps, out)
+    with pytest.raises(dn.DnError):
+        model.denoise_capture(lat, f32_dev(ctx), ts, 1, 5, 7.5, [2], None)
+    torch.cuda.synchronize()
+    assert torch.equal(lat, before)
+    assert not out.float().abs().sum().item()
+    # n_steps = 0: a capture at start_step is the input latent
+    model.denoise_capture(lat, f32_dev(ctx), ts, 4, 0, 7.5, [4], out)
+    torch.cuda.synchronize()
+    assert np.array_equal(_bf16_bits(out[0]), _bf16_bits(lat.to(torch.bfloat16)))

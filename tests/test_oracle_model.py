@@ -18,6 +18,7 @@ import os
 
 import numpy as np
 import pytest
+import torch
 
 from oracle import layers as L, lookup, sampler, schedule as S, topology as T, unet
 from paper_2511_06724_amd import workloads as Wk
@@ -350,3 +351,35 @@ def test_lookup_batch_against_brute_force_and_invariants():
     perm = rng.permutation(6)
     idx2, _ = lookup.top1_batch(qs[perm], cache)
     assert np.array_equal(idx2, idx[perm])
+
+
+# ----------------------------------------------------------------------------- cache write
+
+def test_bf16_round_exact_cases_and_torch():
+    one = 1.0
+    u = 2.0 ** -7  # bf16 spacing at 1
+    xs = np.array([one, one + u / 2, one + 3 * u / 2, one + u / 2 + 2.0 ** -20, -(one + u / 2), 3.0e38,
+                   2.0 ** -130, -0.0, one + u / 2 - 2.0 ** -23], np.float32)
+    want = np.array([one, one, one + 2 * u, one + u, -one, np.float32(3.0e38), 2.0 ** -130, -0.0, one], np.float32)
+    want[5] = np.frombuffer(np.array([(np.float32(3.0e38).view(np.uint32) + 0x8000) & 0xFFFF0000],
+                                     np.uint32).tobytes(), np.float32)[0]
+    got = sampler.bf16_round(xs)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    rng = np.random.default_rng(3)
+    r = (rng.standard_normal(100_000) * np.exp(rng.uniform(-20, 20, 100_000))).astype(np.float32)
+    ref = torch.from_numpy(r).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(sampler.bf16_round(r).view(np.uint32), ref.view(np.uint32))
+
+
+def test_denoise_capture_is_the_trajectory():
+    cfg = Wk.tiny()
+    Wt = unet.unpack(cfg, _blob(cfg).copy())
+    x, ctx = Wk.latent(cfg, 0), Wk.text_ctx(cfg)
+    ts = S.default_timesteps(10)
+    final, caps = sampler.denoise_capture(cfg, Wt, x, ctx, ts, 2, 3, 7.5, [2, 3, 5])
+    x3 = sampler.denoise(cfg, Wt, x, ctx, ts, 2, 1, 7.5)
+    assert np.array_equal(caps[0], sampler.bf16_round(x))
+    assert np.array_equal(caps[1], sampler.bf16_round(x3))
+    assert np.array_equal(caps[2], sampler.bf16_round(final))
+    with pytest.raises(ValueError):
+        sampler.denoise_capture(cfg, Wt, x, ctx, ts, 2, 3, 7.5, [6])
