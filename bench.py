@@ -247,6 +247,20 @@ def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, per_k=2
         dt = (time.perf_counter() - t0) / per_k
         out["images_per_s_by_k"][str(k)] = round(1.0 / dt, 4)
         print(f"[bench] ac k={k}: {1.0 / dt:.3f} images/s", file=sys.stderr, flush=True)
+    # cache write (Sec. 4.7): a full 50-step run that stores its latents at K = 5 .. 25
+    # as bf16 slots of the cache's latent table, against the same run without stores
+    caps = [5, 10, 15, 20, 25]
+    for store in (False, True):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(per_k):
+            if store:
+                model.denoise_capture(lat, ctx, ts, 0, 50, 7.5, caps, lat_cache[:len(caps)])
+            else:
+                model.denoise(lat, ctx, ts, 0, 50, 7.5)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / per_k
+        out["cache_write_images_per_s" if store else "no_write_images_per_s"] = round(1.0 / dt, 4)
     del lat_cache
     return out
 
