@@ -272,7 +272,8 @@ __global__ __launch_bounds__(BatchCfg<KS>::kWaves * 64) void scan_mfma_kernel(co
   const int tiles = (n + 15) / 16;
   const int stride = gridDim.x * NW;
 
-  // the lane's 16-byte slices of row tile * 16 + r16 (past the end: the last row, not scored)
+  // the lane's 16-byte slices of row tile * 16 + r16 (past the end: the last row, not scored);
+  // tile < tiles + 2 * stride keeps tile * 16 + 15 below 2^31 for n < 2^31 - 64
   auto load = [&](uint4 (&a)[KS], int tile) {
     const int row = tile * 16 + r16;
     const uint16_t* src = cache + (long long)(row < n ? row : n - 1) * dim + 8 * grp;
@@ -322,14 +323,17 @@ __global__ __launch_bounds__(BatchCfg<KS>::kWaves * 64) void scan_mfma_kernel(co
 
   const int first = blockIdx.x * NW + w;
   if constexpr (BatchCfg<KS>::kTwoSets) {
+    // The look-ahead loads are unconditional (a tile past the end reads the last row,
+    // in bounds, and is never scored): inside a branch they would make the compiler's
+    // wait counts assume the worst case, so scoring a tile would wait for the next one.
     uint4 a0[KS], a1[KS];
-    if (first < tiles) load(a0, first);
+    load(a0, first);
     for (int tile = first; tile < tiles; tile += 2 * stride) {
       const int t1 = tile + stride;
-      if (t1 < tiles) load(a1, t1);
+      load(a1, t1);
       score(a0, tile);
       if (t1 >= tiles) break;
-      if (t1 + stride < tiles) load(a0, t1 + stride);
+      load(a0, t1 + stride);
       score(a1, t1);
     }
   } else {
