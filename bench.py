@@ -227,6 +227,8 @@ def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, per_k=2
     """Approximate caching: lookup + latent fetch + resume at k for 50 - k steps, per_k
     planted queries per k (each a cosine 0.8-0.95 neighbour of a random cache row)."""
     cache, qd, rows, fig = lookup_timing(torch, dn, n_entries, dim, max(4, per_k))
+    if per_k > 64:
+        raise ValueError("at most 64 queries per k (one batched search)")
     # cached latents: 100,000 x 4 x 128 x 128 bf16 = 13.1 GB, drawn on the device
     g = torch.Generator(device="cuda").manual_seed(8)
     lat_cache = torch.empty((n_entries, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda",
@@ -236,11 +238,13 @@ def ac_sweep(torch, dn, model, cfg, ctx, ts, n_entries=100_000, dim=768, per_k=2
     lat = torch.empty((cfg.batch, cfg.latent_c, cfg.latent_h, cfg.latent_w), device="cuda")
     out = dict(fig)
     out.update({"queries_per_k": per_k, "images_per_s_by_k": {}})
+    qbatch = torch.stack(qd[:per_k])
     for k in (0, 5, 10, 15, 20, 25):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for q in qd[:per_k]:
-            idx, _ = dn.ac_lookup(q, cache)
+        # the k's queries in one batched search, then fetch + resume per query
+        idxs, _ = dn.ac_lookup_batch(qbatch, cache)
+        for idx in idxs:
             dn.ac_fetch_latent(lat_cache, idx, lat)
             model.denoise(lat, ctx, ts, k, 50 - k, 7.5)
         torch.cuda.synchronize()

@@ -190,13 +190,13 @@ def _bf16_bits(t):
     return t.contiguous().view(torch.int16).cpu().numpy()
 
 
-@pytest.mark.parametrize("dtype", [W.DN_FP32, W.DN_BF16])
-def test_capture_is_the_run_rounded_to_bf16(dtype):
+@pytest.mark.parametrize("dtype,batch", [(W.DN_FP32, 1), (W.DN_BF16, 1), (W.DN_FP32, 2)])
+def test_capture_is_the_run_rounded_to_bf16(dtype, batch):
     """dn_denoise_capture leaves the run bitwise unchanged; each slot is bitwise the
     bf16 rounding of the latent after K iterations of the same library; against the
     oracle's captured trajectory within the trajectory bar."""
-    announce(f"capture dtype={dtype}")
-    cfg = W.tiny(dtype)
+    announce(f"capture dtype={dtype} batch={batch}")
+    cfg = W.tiny(dtype).with_(batch=batch)
     model, Wt = _model(cfg)
     x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
     cd = f32_dev(ctx)
