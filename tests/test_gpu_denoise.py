@@ -7,7 +7,10 @@ Bars (relative L2 over the whole tensor, oracle = reference):
 * bf16 mode, the tiny denoiser's free-running 10-step trajectory: final latent
   within 5e-2;
 * resuming at step k (approximate caching, Sec. 2.1) is bitwise equal to the
-  uninterrupted run, and every result is bitwise reproducible.
+  uninterrupted run, and every result is bitwise reproducible;
+* the cache write (dn_denoise_capture, Sec. 4.7) leaves the run bitwise unchanged,
+  each slot is bitwise the bf16 rounding of the library's own state after K
+  iterations, and within 2e-3 (fp32) / 5e-2 (bf16) of the oracle's rounded state.
 """
 
 import numpy as np
@@ -150,8 +153,9 @@ def test_sd15_level_bf16_step():
 
 def test_sdxl_step_properties():
     """Full SD-XL shapes (2.56 B parameters, 128x128 latent, batch 2 with guidance):
-    outputs finite and bitwise reproducible, resume at k bitwise equal to the full run."""
-    announce("sdxl properties: finite, deterministic, resume")
+    outputs finite and bitwise reproducible, resume at k bitwise equal to the full run,
+    cache-write slots bitwise the run's rounded states."""
+    announce("sdxl properties: finite, deterministic, resume, cache write")
     cfg = W.sdxl(W.DN_BF16)
     _CACHE.clear()
     g = torch.Generator(device=DEV).manual_seed(11)
@@ -178,9 +182,19 @@ def test_sdxl_step_properties():
     b = x.clone()
     model.denoise(b, ctx, ts, 0, 1, 7.5)
     model.denoise(b, ctx, ts, 1, 2, 7.5)
+    # cache write at full size: the run is unchanged and the slots are its states rounded
+    c = x.clone()
+    slots = torch.empty((2, 1, 4, 128, 128), device=DEV, dtype=torch.bfloat16)
+    model.denoise_capture(c, ctx, ts, 0, 3, 7.5, [1, 3], slots)
     torch.cuda.synchronize()
     assert torch.isfinite(a).all()
     assert torch.equal(a, b)
+    assert torch.equal(c, a)
+    one = x.clone()
+    model.denoise(one, ctx, ts, 0, 1, 7.5)
+    torch.cuda.synchronize()
+    assert torch.equal(slots[0], one.to(torch.bfloat16))
+    assert torch.equal(slots[1], a.to(torch.bfloat16))
     model.close()
 
 
