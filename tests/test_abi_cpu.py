@@ -115,3 +115,15 @@ def test_one_hip_runtime_per_process():
     process, so torch streams and allocations are valid in the library)."""
     maps = {l.split()[-1] for l in open("/proc/self/maps") if "libamdhip64" in l}
     assert len(maps) == 1, maps
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark is one GPU's throughput; --gpus N > 1 exits with a message before
+    touching a device."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
