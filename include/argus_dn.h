@@ -150,10 +150,15 @@ dn_status dn_weight_count(const dn_config* cfg, size_t* n_floats);
 dn_status dn_weight_table(const dn_config* cfg, int64_t* numel, int32_t* fan_in, int32_t* kind,
                           size_t capacity, size_t* n_tensors);
 
-/* Builds a denoiser: validates cfg, copies the fp32 blob (n_floats values,
- * host or device memory per `weights_location`) and repacks it on the GPU
- * into kernel layouts in the configured dtype. The caller keeps ownership of
- * the blob. Synchronous. On success *out receives the handle. */
+/* Builds a denoiser, i.e. one loaded model of a GPU worker (Sec. 4.5: a worker
+ * serves one model variant at a time; Table 3 sizes the UNets): validates cfg,
+ * copies the fp32 blob (n_floats values, host or device memory per
+ * `weights_location`; n_floats must equal dn_weight_count) and repacks it on the
+ * GPU into kernel layouts in the configured dtype. The caller keeps ownership of
+ * the blob. Synchronous. On success *out receives the handle, which owns the
+ * packed weights and the per-call workspace (freed by dn_destroy); on error
+ * *out is untouched and nothing stays allocated. DN_EUNSUPPORTED when the
+ * current device is not gfx950. */
 dn_status dn_create(const dn_config* cfg, const float* weights, size_t n_floats, int32_t weights_location,
                     dn_handle** out);
 
@@ -315,14 +320,28 @@ dn_status dn_op_linear_vt(int32_t dtype, const void* x, const void* w, const flo
 /* GroupNorm (Wu & He 2018) over NHWC x [n][HW][C] with G groups: biased
  * variance, statistics from fp32 partial sums merged in fp64,
  * y = x_hat * gamma[c] + beta[c], then SiLU if silu != 0. gamma, beta fp32 [C];
- * C % G == 0 and C a multiple of 8. Synchronous (allocates its workspace). */
+ * C % G == 0 and C a multiple of 16 bytes of elements. Asynchronous. Its partial sums
+ * live in the per-device workspace of the single-kernel entry points (grown on
+ * first need; growing it synchronises the device). */
 dn_status dn_op_groupnorm(int32_t dtype, const void* x, void* y, int32_t n, int32_t HW, int32_t C, int32_t G,
-                          const float* gamma, const float* beta, float eps, int32_t silu);
+                          const float* gamma, const float* beta, float eps, int32_t silu, void* stream);
 
 /* LayerNorm over the last axis: x fp32 [M][C] (the residual stream), y [M][C]
  * in `dtype`; C a multiple of 4, at most 2048. Asynchronous. */
 dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int32_t C, const float* gamma,
                           const float* beta, float eps, void* stream);
+
+/* LayerNorm that first completes a residual-stream update whose GEMM split K into
+ * nsplit fp32 partial slabs (the transformer block's out-projection or FF-out feeding
+ * the next LayerNorm, Table 3's SD-XL blocks): for every row,
+ *   x = (resid ? x : 0) + bias + slabs[0] + ... + slabs[nsplit-1]   (fp32, in this order)
+ * is written back to x, then y = LayerNorm(x) * gamma + beta as in dn_op_layernorm.
+ * x fp32 [M][C] (in/out), slabs fp32 [nsplit][M][C], bias fp32 [C] or NULL, y [M][C]
+ * in `dtype`; 1 <= nsplit <= 8; C a multiple of 4, at most 2048; x, slabs, bias, gamma
+ * and beta 16-byte aligned. Asynchronous. */
+dn_status dn_op_layernorm_slabs(int32_t dtype, float* x, void* y, int64_t M, int32_t C, const float* gamma,
+                                const float* beta, float eps, const float* slabs, int32_t nsplit, const float* bias,
+                                int32_t resid, void* stream);
 
 void dn_destroy(dn_handle* h); /* NULL-safe; synchronizes the device first */
 

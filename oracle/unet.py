@@ -37,6 +37,23 @@ def unpack(cfg, blob):
     return out
 
 
+def bf16_model_weights(W):
+    """The parameters of the model in bf16 mode: every convolution and linear weight
+    matrix of the UNet body rounded to bf16 (nearest, ties to even; the values stay
+    fp32 arrays, exactly representable); biases, norm scales and shifts, the time MLP
+    (``time.lin*.w``) and the ResBlocks' time projections (``*.temb.w``) are the time
+    embedding's and the norms' parameters, which bf16 mode keeps in fp32. Returns a
+    new dict; W is not modified."""
+    from .sampler import bf16_round
+    out = {}
+    for k, v in W.items():
+        if k.endswith(".w") and not k.startswith("time.") and not k.endswith(".temb.w"):
+            out[k] = bf16_round(v).reshape(v.shape)
+        else:
+            out[k] = v
+    return out
+
+
 def time_embedding(cfg, W, t):
     """temb = lin2(SiLU(lin1(sinusoid(t, C0)))) -> [4 C0]."""
     e = L.timestep_sinusoid(t, cfg.model_channels)

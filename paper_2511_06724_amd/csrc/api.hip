@@ -87,9 +87,38 @@ struct OpDev {
   void* zero = nullptr;
   float* part = nullptr;  // split-K partial slabs, grown on demand
   size_t part_floats = 0;
+  float* gn = nullptr;    // GroupNorm partial sums and per-channel scale / shift, grown on demand
+  size_t gn_floats = 0;
 };
 std::mutex g_op_mu;
 std::vector<OpDev> g_op_dev;
+
+// Grows a per-device buffer of the single-kernel entry points. Work already enqueued
+// may still read the old buffer, so the device is synchronised before it is freed.
+void grow(float** buf, size_t* have, size_t need) {
+  if (need <= *have) return;
+  if (*buf) {
+    DN_HIP(hipDeviceSynchronize());
+    DN_HIP(hipFree(*buf));
+    *buf = nullptr;
+    *have = 0;
+  }
+  DN_HIP(hipMalloc(reinterpret_cast<void**>(buf), need * 4));
+  *have = need;
+}
+
+OpDev& op_dev_locked(int dev) {
+  if ((int)g_op_dev.size() <= dev) g_op_dev.resize(dev + 1);
+  OpDev& d = g_op_dev[dev];
+  if (!d.cus) {
+    hipDeviceProp_t prop;
+    DN_HIP(hipGetDeviceProperties(&prop, dev));
+    DN_HIP(hipMalloc(&d.zero, 256));
+    DN_HIP(hipMemset(d.zero, 0, 256));
+    d.cus = prop.multiProcessorCount;
+  }
+  return d;
+}
 
 template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
   int dev = 0;
@@ -97,27 +126,9 @@ template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
   OpDev w;
   {
     std::lock_guard<std::mutex> lk(g_op_mu);
-    if ((int)g_op_dev.size() <= dev) g_op_dev.resize(dev + 1);
-    OpDev& d = g_op_dev[dev];
-    if (!d.cus) {
-      hipDeviceProp_t prop;
-      DN_HIP(hipGetDeviceProperties(&prop, dev));
-      DN_HIP(hipMalloc(&d.zero, 256));
-      DN_HIP(hipMemset(d.zero, 0, 256));
-      d.cus = prop.multiProcessorCount;
-    }
+    OpDev& d = op_dev_locked(dev);
     const dn::GemmPlan g0 = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, d.cus, p.vt == nullptr, false, p.taps == 9);
-    const size_t need = dn::gemm_workspace_floats(g0, p.M, p.N);
-    if (need > d.part_floats) {
-      if (d.part) {
-        DN_HIP(hipDeviceSynchronize());
-        DN_HIP(hipFree(d.part));
-        d.part = nullptr;
-        d.part_floats = 0;
-      }
-      DN_HIP(hipMalloc(&d.part, need * 4));
-      d.part_floats = need;
-    }
+    grow(&d.part, &d.part_floats, dn::gemm_workspace_floats(g0, p.M, p.N));
     w = d;
   }
   const dn::GemmPlan g = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, w.cus, p.vt == nullptr, false, p.taps == 9);
@@ -455,38 +466,38 @@ dn_status dn_op_linear_vt(int32_t dtype, const void* x, const void* w, const flo
 }
 
 dn_status dn_op_groupnorm(int32_t dtype, const void* x, void* y, int32_t n, int32_t HW, int32_t C, int32_t G,
-                          const float* gamma, const float* beta, float eps, int32_t silu) {
+                          const float* gamma, const float* beta, float eps, int32_t silu, void* stream) {
   return guarded([&] {
     DN_CHECK(is_dtype(dtype), "dn_op_groupnorm: bad dtype");
     DN_CHECK(x && y && gamma && beta, "dn_op_groupnorm: null pointer");
     DN_CHECK(n >= 1 && HW >= 1 && C >= 1 && G >= 1 && C % G == 0, "dn_op_groupnorm: bad sizes");
-    float* ws = nullptr;
+    int dev = 0;
+    DN_HIP(hipGetDevice(&dev));
     const size_t part = dn::groupnorm_workspace_floats(n, HW, C, G);
-    DN_HIP(hipMalloc(&ws, (part + (size_t)2 * n * C) * 4));
-    try {
-      dn::GroupNormParams p;
-      p.x0 = x;
-      p.c0 = C;
-      p.n = n;
-      p.HW = HW;
-      p.G = G;
-      p.gamma = gamma;
-      p.beta = beta;
-      p.eps = eps;
-      p.silu = silu;
-      p.y = y;
-      p.partial = ws;
-      p.stats = ws + part;
-      if (dtype == DN_BF16)
-        dn::groupnorm<dn::bf16>(p, nullptr);
-      else
-        dn::groupnorm<float>(p, nullptr);
-      DN_HIP(hipDeviceSynchronize());
-    } catch (...) {
-      (void)hipFree(ws);
-      throw;
+    float* ws = nullptr;
+    {
+      std::lock_guard<std::mutex> lk(g_op_mu);
+      OpDev& d = op_dev_locked(dev);
+      grow(&d.gn, &d.gn_floats, part + (size_t)2 * n * C);
+      ws = d.gn;
     }
-    DN_HIP(hipFree(ws));
+    dn::GroupNormParams p;
+    p.x0 = x;
+    p.c0 = C;
+    p.n = n;
+    p.HW = HW;
+    p.G = G;
+    p.gamma = gamma;
+    p.beta = beta;
+    p.eps = eps;
+    p.silu = silu;
+    p.y = y;
+    p.partial = ws;
+    p.stats = ws + part;
+    if (dtype == DN_BF16)
+      dn::groupnorm<dn::bf16>(p, as_stream(stream));
+    else
+      dn::groupnorm<float>(p, as_stream(stream));
   });
 }
 
@@ -499,6 +510,23 @@ dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int
       dn::layernorm<dn::bf16>(x, static_cast<dn::bf16*>(y), M, C, gamma, beta, eps, as_stream(stream));
     else
       dn::layernorm<float>(x, static_cast<float*>(y), M, C, gamma, beta, eps, as_stream(stream));
+  });
+}
+
+dn_status dn_op_layernorm_slabs(int32_t dtype, float* x, void* y, int64_t M, int32_t C, const float* gamma,
+                                const float* beta, float eps, const float* slabs, int32_t nsplit, const float* bias,
+                                int32_t resid, void* stream) {
+  return guarded([&] {
+    DN_CHECK(is_dtype(dtype), "dn_op_layernorm_slabs: bad dtype");
+    DN_CHECK(x && y && gamma && beta && slabs, "dn_op_layernorm_slabs: null pointer");
+    DN_CHECK(nsplit >= 1 && nsplit <= 8, "dn_op_layernorm_slabs: nsplit must be in [1, 8]");
+    DN_CHECK(resid == 0 || resid == 1, "dn_op_layernorm_slabs: resid must be 0 or 1");
+    if (dtype == DN_BF16)
+      dn::layernorm_reduce<dn::bf16>(x, static_cast<dn::bf16*>(y), M, C, gamma, beta, eps, slabs, nsplit, bias,
+                                     resid != 0, as_stream(stream));
+    else
+      dn::layernorm_reduce<float>(x, static_cast<float*>(y), M, C, gamma, beta, eps, slabs, nsplit, bias,
+                                  resid != 0, as_stream(stream));
   });
 }
 

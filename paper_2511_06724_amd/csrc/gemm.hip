@@ -254,17 +254,11 @@ template <typename T, bool CONV> void dispatch(const GemmParams& p, const GemmPl
 
 }  // namespace
 
-// Tile choice, from measurements on MI355X (SD-XL shapes, bf16, weights streamed
-// from HBM as in the denoise loop):
-//  - tall problems (M >= 8192 rows) go to the direct-to-LDS kernel: 256 x 256 tiles
-//    when every CU gets at least one (the 128 x 128 latent convolutions), else
-//    128 x 256 tiles, three LDS stages when the grid is a single round (N <= 768);
-//  - otherwise the register-staged kernel: 64 x 64 tiles when there are fewer
-//    128 x 128 tiles than CUs (the M = 2048, N = 1280 projections; GEGLU needs
-//    64-column value/gate pairs per wave, i.e. a block width of at least 128), else
-//    128 x 128 tiles with two resident workgroups per CU;
-//  - fp32 (the check mode), narrow outputs (N < 128) and K not a multiple of 64 take
-//    the register-staged kernel.
+// Tile choice of the register-staged kernel (fp32, the check mode, and bf16 shapes the
+// fragment layout does not take: N % 32 != 0 or K % 64 != 0, e.g. conv_in and the
+// output head): 64 x 64 tiles when there are fewer 128 x 128 tiles than CUs (GEGLU
+// needs 64-column value/gate pairs per wave, i.e. a block width of at least 128), else
+// 128 x 128 tiles with two resident workgroups per CU.
 // Fragment-B kernel (bf16 weights in fragment order). Three tile variants share a CU
 // between several workgroups: 128 x 256 (two per CU), 128 x 128 (two) and 64 x 128
 // (four); five-wave 64 x 160 and 128 x 160 tiles run one workgroup per CU (the M = 2048,
@@ -337,11 +331,6 @@ template <typename T>
 GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce, bool conv) {
   if (sizeof(T) == 2 && gemm_frag_layout(N, K)) return frag_plan(M, N, K, geglu, cus, allow_split, fused_reduce, conv);
   const long long t128 = (long long)ceil_div(M, 128) * ceil_div(N, 128);
-  if (sizeof(T) == 2 && N >= 128 && K % 64 == 0 && M >= 8192) {
-    const long long t256 = (long long)ceil_div(M, 256) * ceil_div(N, 256);
-    if (M >= 16384 && t256 >= cus) return GemmPlan{256, 256, 1, 2, 4, 2};
-    return GemmPlan{128, 256, 1, 2, 4, N <= 768 ? 3 : 2};
-  }
   if (!geglu && t128 < cus) return GemmPlan{64, 64, 0};
   return GemmPlan{128, 128, 0};
 }
@@ -356,7 +345,7 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
   DN_CHECK(p.taps == 1 || (p.c0 + p.c1) % BK == 0, "gemm: conv channels must be a multiple of the K tile");
   DN_CHECK(p.a0 && p.b && p.out && (p.c1 == 0 || p.a1), "gemm: null operand");
   DN_CHECK(!p.geglu || (p.N % 64 == 0), "gemm: GEGLU needs N % 64 == 0");
-  DN_CHECK(!p.geglu || (g.dma ? (g.bn / g.wgn) % 64 == 0 : (g.bn / 2) % 64 == 0),
+  DN_CHECK(!p.geglu || (g.bn / 2) % 64 == 0,
            "gemm: GEGLU needs 64-column value/gate pairs per wave");
   DN_CHECK(p.ldb % (16 / (int)sizeof(T)) == 0 && p.lda0 % (16 / (int)sizeof(T)) == 0 &&
                (p.c1 == 0 || p.lda1 % (16 / (int)sizeof(T)) == 0),
@@ -364,11 +353,6 @@ template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStrea
   if (g.frag) {
     DN_CHECK(sizeof(T) == 2, "gemm: the fragment-B kernel is bf16 only");
     gemm_bf16_frag(p, g, s);
-    return;
-  }
-  if (g.dma) {
-    DN_CHECK(sizeof(T) == 2, "gemm: the direct-to-LDS kernel is bf16 only");
-    gemm_bf16_dma(p, g, s);
     return;
   }
   if (p.taps == 9)

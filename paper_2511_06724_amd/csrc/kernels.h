@@ -37,7 +37,7 @@ struct GemmParams {
   int ldo = 0, out_f32 = 0;
   int n_store = 0;  // output columns written
   int geglu = 0;
-  const void* zero16 = nullptr;  // >= 16 zero bytes (implicit-conv padding reads, direct-to-LDS path)
+  const void* zero16 = nullptr;  // >= 16 zero bytes (implicit-conv padding reads of the fragment-B kernel)
   // Transposed V output: columns n >= vt_col0 (the V projection of an attention,
   // heads of vt_dp columns) are written to vt[sample][head][d][token] with token
   // stride 1 and d stride vt_ld; rows are tokens, vt_seq per sample.
@@ -54,10 +54,8 @@ struct GemmParams {
 // Block tile (bm x bn) of one GEMM launch and the kernel that runs it.
 struct GemmPlan {
   int bm, bn;
-  int dma = 0;  // 1: bf16 direct-to-LDS kernel (gemm_dma.hip), else the register-staged kernel
-  int wgm = 2, wgn = 2;  // direct-to-LDS kernel: wave grid over the block tile
-  int stages = 2;        // direct-to-LDS / fragment-B kernels: LDS pipeline depth
-  int frag = 0;          // 1: bf16 fragment-B kernel (gemm_frag.hip)
+  int stages = 2;        // fragment-B kernel: LDS pipeline depth
+  int frag = 0;          // 1: bf16 fragment-B kernel (gemm_frag.hip), else the register-staged kernel
   int split = 1;         // fragment-B kernel: K split in this many ranges (fp32 partials + reduce)
 };
 constexpr int kMaxSplit = 8;
@@ -68,7 +66,6 @@ template <typename T>
 GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split = true, bool fused_reduce = false,
                    bool conv = false);
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s);
-void gemm_bf16_dma(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 // bf16 weight matrices [N][K] with gemm_frag_layout(N, K) are stored in MFMA fragment
 // order (gemm_frag.hip) and multiplied by the fragment-B kernel; every other shape,

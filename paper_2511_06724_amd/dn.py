@@ -23,8 +23,8 @@ MAX_LEVELS = 4
 
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_denoise_capture", "dn_unet_eps", "ac_lookup",
             "ac_lookup_batch", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
-            "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_linear_vt", "dn_destroy",
-            "dn_last_error")
+            "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_layernorm_slabs", "dn_op_linear_vt",
+            "dn_destroy", "dn_last_error")
 
 
 class DnError(RuntimeError):
@@ -76,8 +76,9 @@ def _load():
         "dn_op_conv3x3": [I32, P, I32, I32, I32, I32, I32, I32, P, P, P, P, P, I32, I32, P],
         "dn_op_attention": [I32, P, I32, P, I32, P, I32, P, I32, I32, I32, I32, I32, I32, F32, P],
         "dn_op_linear_vt": [I32, P, P, P, P, I64, I32, I32, I32, P, I32, I32, I32, I32, P],
-        "dn_op_groupnorm": [I32, P, P, I32, I32, I32, I32, P, P, F32, I32],
+        "dn_op_groupnorm": [I32, P, P, I32, I32, I32, I32, P, P, F32, I32, P],
         "dn_op_layernorm": [I32, P, P, I64, I32, P, P, F32, P],
+        "dn_op_layernorm_slabs": [I32, P, P, I64, I32, P, P, F32, P, I32, P, I32, P],
         "dn_destroy": [P],
         "dn_last_error": [],
     }
@@ -270,9 +271,15 @@ def op_linear_vt(dtype, x, w, bias, y, M, N, K, vt_col0, vt, heads, head_stride,
                                head_stride, seq, vt_ld, _stream(stream)))
 
 
-def op_groupnorm(dtype, x, y, n, HW, Cc, G, gamma, beta, eps, silu):
-    _check(lib.dn_op_groupnorm(dtype, _ptr(x), _ptr(y), n, HW, Cc, G, _ptr(gamma), _ptr(beta), eps, int(silu)))
+def op_groupnorm(dtype, x, y, n, HW, Cc, G, gamma, beta, eps, silu, stream=None):
+    _check(lib.dn_op_groupnorm(dtype, _ptr(x), _ptr(y), n, HW, Cc, G, _ptr(gamma), _ptr(beta), eps, int(silu),
+                               _stream(stream)))
 
 
 def op_layernorm(dtype, x, y, M, Cc, gamma, beta, eps, stream=None):
     _check(lib.dn_op_layernorm(dtype, _ptr(x), _ptr(y), M, Cc, _ptr(gamma), _ptr(beta), eps, _stream(stream)))
+
+
+def op_layernorm_slabs(dtype, x, y, M, Cc, gamma, beta, eps, slabs, nsplit, bias=None, resid=True, stream=None):
+    _check(lib.dn_op_layernorm_slabs(dtype, _ptr(x), _ptr(y), M, Cc, _ptr(gamma), _ptr(beta), eps, _ptr(slabs), nsplit,
+                                     _ptr(bias), int(resid), _stream(stream)))

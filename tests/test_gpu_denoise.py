@@ -151,29 +151,58 @@ def test_sd15_level_bf16_step():
     assert e <= 2e-2
 
 
-def test_sdxl_step_properties():
-    """Full SD-XL shapes (2.56 B parameters, 128x128 latent, batch 2 with guidance):
-    outputs finite and bitwise reproducible, resume at k bitwise equal to the full run,
-    cache-write slots bitwise the run's rounded states."""
-    announce("sdxl properties: finite, deterministic, resume, cache write")
+def _sdxl_model(seed=11):
     cfg = W.sdxl(W.DN_BF16)
     _CACHE.clear()
-    g = torch.Generator(device=DEV).manual_seed(11)
-    table = dn.weight_table(cfg)
-    n = sum(t[0] for t in table)
-    blob = torch.empty(n, device=DEV)
-    off = 0
-    for numel, fan, kind in table:
-        v = blob[off:off + numel]
-        if kind in (0, 1):
-            v.normal_(0.0, fan ** -0.5, generator=g)
-        elif kind == 2:
-            v.normal_(1.0, 0.1, generator=g)
-        else:
-            v.normal_(0.0, 0.1, generator=g)
-        off += numel
-    model = dn.Denoiser(cfg, blob)
+    blob = W.weight_blob_device(dn.weight_table(cfg), seed, DEV)
+    return cfg, blob, dn.Denoiser(cfg, blob)
+
+
+@pytest.mark.timeout(900)
+def test_sdxl_teacher_forced_step_vs_oracle():
+    """The headline SD-XL-shaped UNet (2.56 B parameters, 128x128 latent, guidance batch 2,
+    bf16: 10-deep C = 1280 transformer stacks, 2560 / 1920-channel concatenation
+    ResBlocks, the three-slab split-K LayerNorm, M = 32768 convolutions) against the
+    oracle on one teacher-forced iteration at t = 981. The bar (raw UNet output within
+    2e-2 relative L2) is taken against the oracle evaluating the bf16 model, i.e. the
+    seeded weights rounded to bf16 as dn_create stores them (``unet.bf16_model_weights``),
+    in fp32 arithmetic; at this depth the rounding of the weights alone moves the fp32
+    output by about 2e-2. The distance to the oracle on the unrounded weights is
+    reported and bounded loosely (3e-2); guided eps and the DDIM update are reported."""
+    announce("sdxl bf16 teacher-forced step vs oracle (oracle ~13.5 TFLOP on the host)")
+    cfg, blob, model = _sdxl_model()
+    host_blob = blob.cpu().numpy()
     del blob
+    x, ctx = W.latent(cfg, 0), W.text_ctx(cfg)
+    raw, guided = _eps(model, cfg, x, 981, ctx, 7.5)
+    lat = f32_dev(x)
+    model.denoise(lat, f32_dev(ctx), np.array([981, 961], np.int32), 0, 1, 7.5)
+    torch.cuda.synchronize()
+    x_next = lat.cpu().numpy()
+    model.close()
+    torch.cuda.empty_cache()
+    announce("  GPU step done; oracle step running")
+    Wt = unet.unpack(cfg, host_blob)
+    ref_raw, ref_eps, ref_next = sampler.step(cfg, unet.bf16_model_weights(Wt), x, ctx, 981, 961, 7.5)
+    e_raw, e_eps, e_next = rel_l2(raw, ref_raw), rel_l2(guided, ref_eps), rel_l2(x_next, ref_next)
+    announce(f"  vs oracle on the bf16 model: rel-L2 raw {e_raw:.3e}  guided {e_eps:.3e}  x_next {e_next:.3e}")
+    announce("  oracle on the unrounded weights running")
+    ref32_raw, _, _ = sampler.step(cfg, Wt, x, ctx, 981, 961, 7.5)
+    e32 = rel_l2(raw, ref32_raw)
+    announce(f"  vs oracle on the unrounded weights: rel-L2 raw {e32:.3e} "
+             f"(weight rounding alone: {rel_l2(ref_raw, ref32_raw):.3e})")
+    assert np.isfinite(raw).all() and np.isfinite(x_next).all()
+    assert e_raw <= 2e-2
+    assert e32 <= 3e-2
+
+
+def test_sdxl_step_properties():
+    """Full SD-XL shapes: outputs finite and bitwise reproducible, resume at k bitwise
+    equal to the full run, cache-write slots bitwise the run's rounded states."""
+    announce("sdxl properties: finite, deterministic, resume, cache write")
+    cfg, blob, model = _sdxl_model()
+    del blob
+    g = torch.Generator(device=DEV).manual_seed(12)
     x = torch.randn((1, 4, 128, 128), device=DEV, generator=g)
     ctx = torch.randn((2, 77, 2048), device=DEV, generator=g)
     ts = S.default_timesteps(50)

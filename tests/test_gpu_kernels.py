@@ -35,14 +35,15 @@ def _rng(seed):
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280),
                                    (2048, 2048, 128), (8192, 512, 256), (300, 1280, 2560), (77, 96, 1920),
-                                   (1000, 640, 5120), (129, 256, 704), (2000, 1248, 1280), (8000, 608, 2560)])
+                                   (1000, 640, 5120), (129, 256, 704), (2000, 1248, 1280), (8000, 608, 2560),
+                                   (8192, 200, 256)])
 def test_linear(dtype, M, N, K):
     """Shapes cover every tile plan: in fp32 the register-staged 64 x 64 / 128 x 128
     tiles; in bf16 the row-major kernels for N % 32 != 0 (N = 200) and the fragment-B
     kernel with 128 x 128 and 128 x 256 tiles, with and without split-K (few tiles and
     long K: 300 x 1280 x 2560, 1000 x 640 x 5120), the five-wave 64 x 160 and 128 x 160
     tiles (2000 x 1248 x 1280, 8000 x 608 x 2560: one tile per CU, ragged last row tile
-    and column tile), ragged M and N tails. Outputs: bf16 / fp32 without residual, fp32
+    and column tile), ragged M and N tails; a tall row-major case (8192 x 200 x 256). Outputs: bf16 / fp32 without residual, fp32
     with an fp32 residual, and the op's dtype with a residual in that dtype."""
     announce(f"linear dtype={dtype} M={M} N={N} K={K}")
     r = _rng(M + N + K)
@@ -175,8 +176,8 @@ def test_attention(dtype, B, heads, Sq, Skv, d):
                                               (2048, 1024, 20, 64, 1280)])
 def test_linear_vt(dtype, M, seq, heads, dp, K):
     """Attention input projection: Q, K columns to y, V columns transposed per head
-    into vt[sample][head][d][token] (the last two shapes are the SD-XL QKV projections,
-    the 8192-row one on the direct-to-LDS kernel)."""
+    into vt[sample][head][d][token] (the last two shapes are the SD-XL QKV projections
+    at the 64x64 and 32x32 levels, on the fragment-B kernel)."""
     announce(f"linear_vt dtype={dtype} M={M} seq={seq} heads={heads} dp={dp} K={K}")
     P = heads * dp
     N = 3 * P
@@ -211,6 +212,7 @@ def test_groupnorm(dtype, n, HW, C, G, silu):
     b = (0.1 * r.standard_normal(C)).astype(np.float32)
     y = torch.empty((n, HW, C), device=DEV, dtype=tdtype(dtype))
     dn.op_groupnorm(dtype, x, y, n, HW, C, G, f32_dev(g), f32_dev(b), 1e-5, silu)
+    torch.cuda.synchronize()
     ref = L.group_norm(xh.transpose(0, 2, 1)[..., None], G, g.astype(np.float64), b.astype(np.float64), 1e-5)
     ref = ref[..., 0].transpose(0, 2, 1)
     if silu:
@@ -231,6 +233,47 @@ def test_layernorm(dtype, M, C):
     torch.cuda.synchronize()
     ref = L.layer_norm(x.astype(np.float64), g.astype(np.float64), b.astype(np.float64), 1e-5)
     assert rel_l2(host(y), ref) < (2e-6 if dtype == dn.DN_FP32 else TOL[dtype])
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("M,C,nsplit,bias,resid", [(2048, 1280, 3, True, True), (2048, 1280, 2, True, False),
+                                                   (8192, 640, 4, True, True), (301, 320, 1, False, True),
+                                                   (77, 2048, 8, True, True)])
+def test_layernorm_slabs(dtype, M, C, nsplit, bias, resid):
+    """The LayerNorm that completes a split-K residual update: x <- (x if resid) + bias +
+    sum of the fp32 slabs, written back, then normalised. 2048 x 1280 with three slabs is
+    the FF-out of a 32x32 SD-XL block feeding the next block's first LayerNorm; two
+    slabs without residual is proj_in; the widest row (C = 2048) with eight slabs."""
+    announce(f"layernorm slabs dtype={dtype} M={M} C={C} nsplit={nsplit} bias={bias} resid={resid}")
+    r = _rng(M + C + nsplit)
+    x = (0.5 + 2.0 * r.standard_normal((M, C))).astype(np.float32)
+    slabs = r.standard_normal((nsplit, M, C)).astype(np.float32)
+    bv = r.standard_normal(C).astype(np.float32)
+    g = (1 + 0.1 * r.standard_normal(C)).astype(np.float32)
+    b = (0.1 * r.standard_normal(C)).astype(np.float32)
+    xd = f32_dev(x)
+    y = torch.empty((M, C), device=DEV, dtype=tdtype(dtype))
+    dn.op_layernorm_slabs(dtype, xd, y, M, C, f32_dev(g), f32_dev(b), 1e-5, f32_dev(slabs), nsplit,
+                          f32_dev(bv) if bias else None, resid)
+    torch.cuda.synchronize()
+    full = (x.astype(np.float64) if resid else 0.0) + slabs.astype(np.float64).sum(axis=0)
+    if bias:
+        full = full + bv
+    # the rebuilt residual row: fp32 sums of at most 10 terms of size ~3
+    assert rel_l2(host(xd), full) < 1e-6
+    ref = L.layer_norm(full, g.astype(np.float64), b.astype(np.float64), 1e-5)
+    assert rel_l2(host(y), ref) < (2e-6 if dtype == dn.DN_FP32 else TOL[dtype])
+
+
+def test_layernorm_slabs_argument_errors():
+    x = torch.zeros((4, 64), device=DEV)
+    y = torch.zeros((4, 64), device=DEV)
+    g = torch.ones(64, device=DEV)
+    for ns in (0, 9):
+        with pytest.raises(dn.DnError):
+            dn.op_layernorm_slabs(dn.DN_FP32, x, y, 4, 64, g, g, 1e-5, x, ns)
+    with pytest.raises(dn.DnError):
+        dn.op_layernorm_slabs(dn.DN_FP32, x, y, 4, 64, g, g, 1e-5, None, 1)
 
 
 # ----------------------------------------------------------------------------- SD-XL shapes, sampled

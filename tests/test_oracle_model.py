@@ -80,17 +80,37 @@ def test_weight_table_order_head_and_tail():
 
 # ----------------------------------------------------------------------------- schedule / DDIM / CFG
 
+def _golden_abar(name):
+    out = {}
+    for line in open(os.path.join(GOLD, name)):
+        if not line.startswith("#"):
+            t, v = line.split()
+            out[int(t)] = float(v)
+    return out
+
+
 def test_abar_linear_matches_exact_rationals():
     ab = S.alphas_cumprod(S.betas())
-    for line in open(os.path.join(GOLD, "abar_linear.txt")):
-        if line.startswith("#"):
-            continue
-        t, v = line.split()
-        assert abs(ab[int(t)] - float(v)) / float(v) < 1e-11
+    gold = _golden_abar("abar_linear.txt")
+    assert len(gold) == 8
+    for t, v in gold.items():
+        assert abs(ab[t] - v) / v < 1e-11
     assert np.all(np.diff(ab) < 0)
+
+
+def test_abar_scaled_linear_matches_extended_precision():
+    """Scaled-linear branch (beta = square of a linear ramp of square roots) against
+    60-digit decimal products; abar_981 = 5.7755e-3 is the known value of this schedule."""
     sl = S.alphas_cumprod(S.betas(kind=S.SCALED_LINEAR))
-    assert abs(sl[0] - (1 - 0.00085)) < 1e-15
-    assert sl[981] > ab[981]
+    gold = _golden_abar("abar_scaled_linear.txt")
+    assert len(gold) == 8
+    for t, v in gold.items():
+        assert abs(sl[t] - v) / v < 1e-11, (t, sl[t], v)
+    assert abs(sl[981] - 5.7755e-3) < 5e-8
+    assert np.all(np.diff(sl) < 0)
+    # the two schedules share their end points but not their interior
+    ab = S.alphas_cumprod(S.betas())
+    assert abs(sl[0] - ab[0]) < 1e-15 and sl[981] > ab[981]
 
 
 def test_default_timesteps():
@@ -383,3 +403,24 @@ def test_denoise_capture_is_the_trajectory():
     assert np.array_equal(caps[2], sampler.bf16_round(final))
     with pytest.raises(ValueError):
         sampler.denoise_capture(cfg, Wt, x, ctx, ts, 2, 3, 7.5, [6])
+
+
+def test_bf16_model_weights_rounds_exactly_the_gemm_weights():
+    """bf16 mode's parameters: conv / linear weight matrices rounded to bf16, every
+    other tensor (biases, norms, time MLP, ResBlock time projections) unchanged."""
+    cfg = Wk.tiny()
+    blob = Wk.weight_blob([(int(np.prod(s)), f, k) for _, s, k, f in T.tensor_table(cfg)], 3)
+    Wt = unet.unpack(cfg, blob)
+    W16 = unet.bf16_model_weights(Wt)
+    assert W16.keys() == Wt.keys()
+    rounded = [k for k in Wt if not np.array_equal(W16[k], Wt[k])]
+    expect = [k for k in Wt if k.endswith(".w") and not k.startswith("time.") and not k.endswith(".temb.w")]
+    assert sorted(rounded) == sorted(expect) and "conv_in.w" in expect and "down0.0.tx.blk0.ff1.w" in expect
+    for k in expect:
+        bits = W16[k].view(np.uint32)
+        assert np.all(bits & 0xFFFF == 0), k                       # exactly representable in bf16
+        assert W16[k].shape == Wt[k].shape
+        rel = np.abs(W16[k] - Wt[k]) / np.maximum(np.abs(Wt[k]), 1e-30)
+        assert rel.max() <= 2.0 ** -8, k                          # nearest: within half a bf16 ulp
+        assert np.array_equal(unet.bf16_model_weights({k: W16[k]})[k], W16[k])   # idempotent
+    assert W16["time.lin1.w"] is Wt["time.lin1.w"]
