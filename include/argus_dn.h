@@ -16,6 +16,7 @@
  *   dn_denoise_capture                 the same, writing the latent after chosen iterations (cache write)
  *   ac_lookup                          top-1 cosine search over the prompt-embedding cache
  *   ac_lookup_batch                    the same search for many queries in one pass over the cache
+ *   ac_lookup_batch_noalloc            ac_lookup_batch on a stream, results in device memory, no allocation
  *   ac_fetch_latent                    copy cached latent #idx into an fp32 latent buffer
  *   dn_unet_eps                        one UNet evaluation + guidance (per-step check hook)
  *   dn_op_*                            single-kernel entry points (kernel checks, timing)
@@ -234,6 +235,24 @@ dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64
  * overlap on one device race on them. */
 dn_status ac_lookup_batch(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n, int32_t dim,
                           int64_t* out_idx, float* out_score);
+
+/* For callers that cannot allocate — code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation: the search of ac_lookup_batch (same
+ * kernels, same results bit for bit) enqueued on `stream`, with the results in
+ * device memory and the per-workgroup winners in a fixed scratch array of the
+ * library (256 KiB per GPU, held until the process ends). The call allocates
+ * nothing (no hipMalloc, hipFree or pinned host memory) and does not synchronise.
+ * out_idx    device int64 [nq]: first row of maximal cosine per query, -1 when the
+ *            query is zero (or every row is).
+ * out_score  device float [nq] (the cosines) or NULL.
+ * Any nq >= 1 (passes of 64 queries run one after another on `stream`), n >= 1,
+ * dim >= 1 (dim <= 16384 off the matrix-core widths 256/512/768/1024).
+ * Every call on one GPU shares that GPU's scratch: calls that overlap on one GPU
+ * (several streams or threads) race and must be serialised by the caller. Returns
+ * DN_EINVAL before enqueuing anything if the scan would need more scratch than
+ * the library holds. */
+dn_status ac_lookup_batch_noalloc(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n,
+                                  int32_t dim, int64_t* out_idx, float* out_score, void* stream);
 
 /* Copies cached latent #idx of a device bf16 table [n][numel] into the device
  * fp32 latent buffer [numel] (the resume state of Sec. 4.7). Asynchronous. */

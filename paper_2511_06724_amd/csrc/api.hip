@@ -8,7 +8,36 @@
 
 #include "model.h"
 
+// Scratch of the no-allocation batched lookup: the per-workgroup winners of one pass
+// (at most lookup_batch_workspace_bytes(), 256 KiB, which also covers the per-query
+// scan's lookup_workspace_bytes()), then 64 floats that receive the cosines when the
+// caller asks for none. Every GPU the library runs on holds its own copy until the
+// process ends; its device address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchWinnerBytes = 256 * 1024;
+constexpr size_t kScratchBytes = kScratchWinnerBytes + 64 * sizeof(float);
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (looked up on the first call on
+// that device, with the device current; later calls reuse it).
+void* scratch_ptr() {
+  int dev = 0;
+  DN_HIP(hipGetDevice(&dev));
+  DN_CHECK(dev >= 0 && dev < kMaxDevices, "scratch: device ordinal beyond 64");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    DN_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    DN_CHECK(p != nullptr, "scratch: no device address");
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
 
 thread_local std::string g_last_error;
 
@@ -276,6 +305,38 @@ dn_status ac_lookup_batch(const uint16_t* query_embs, int32_t nq, const uint16_t
         out_idx[j0 + j] = idx;
         if (out_score) out_score[j0 + j] = static_cast<volatile float*>(rscore)[j];
       }
+    }
+  });
+}
+
+dn_status ac_lookup_batch_noalloc(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n,
+                                  int32_t dim, int64_t* out_idx, float* out_score, void* stream) {
+  return guarded([&] {
+    DN_CHECK(query_embs && cache_embs && out_idx, "ac_lookup_batch_noalloc: null pointer");
+    DN_CHECK(nq >= 1, "ac_lookup_batch_noalloc: nq must be >= 1");
+    DN_CHECK(n >= 1, "ac_lookup_batch_noalloc: n must be >= 1");
+    DN_CHECK(dim >= 1, "ac_lookup_batch_noalloc: dim must be >= 1");
+    const bool batched = dn::lookup_batch_supported(query_embs, cache_embs, n, dim);
+    const size_t need = batched ? dn::lookup_batch_workspace_bytes() : dn::lookup_workspace_bytes();
+    DN_CHECK(need <= kScratchWinnerBytes, "ac_lookup_batch_noalloc: scan needs " + std::to_string(need) +
+                                              " bytes of scratch, the library holds " +
+                                              std::to_string(kScratchWinnerBytes));
+    DN_CHECK(batched || dim <= 16384, "ac_lookup_batch_noalloc: dim too large for the per-query scan");
+    char* ws = static_cast<char*>(scratch_ptr());
+    float* dummy = reinterpret_cast<float*>(ws + kScratchWinnerBytes);
+    const hipStream_t s = as_stream(stream);
+    long long* idx = reinterpret_cast<long long*>(out_idx);
+    if (batched) {
+      const int mq = dn::lookup_batch_max_queries();
+      for (int j0 = 0; j0 < nq; j0 += mq) {
+        const int m = nq - j0 < mq ? nq - j0 : mq;
+        dn::lookup_batch(query_embs + (size_t)j0 * dim, m, cache_embs, n, dim, ws, idx + j0,
+                         out_score ? out_score + j0 : dummy, s);
+      }
+    } else {
+      for (int j = 0; j < nq; ++j)
+        dn::lookup(query_embs + (size_t)j * dim, cache_embs, n, dim, ws, idx + j, out_score ? out_score + j : dummy,
+                   s);
     }
   });
 }

@@ -22,7 +22,7 @@ ABI_VERSION = 1
 MAX_LEVELS = 4
 
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_denoise_capture", "dn_unet_eps", "ac_lookup",
-            "ac_lookup_batch", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
+            "ac_lookup_batch", "ac_lookup_batch_noalloc", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
             "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_layernorm_slabs", "dn_op_linear_vt",
             "dn_destroy", "dn_last_error")
 
@@ -69,6 +69,7 @@ def _load():
         "dn_unet_eps": [P, P, I32, P, F32, P, P, P],
         "ac_lookup": [P, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
         "ac_lookup_batch": [P, I32, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
+        "ac_lookup_batch_noalloc": [P, I32, P, I64, I32, P, P, P],
         "ac_fetch_latent": [P, I64, I64, I64, P, P],
         "dn_packed_weight_elems": [I32, I32, I32, C.POINTER(I64)],
         "dn_pack_weight": [I32, P, I32, I32, P, P],
@@ -228,6 +229,17 @@ def ac_lookup_batch(queries, cache):
     score = (C.c_float * nq)()
     _check(lib.ac_lookup_batch(_ptr(queries), nq, _ptr(cache), n, dim, idx, score))
     return list(idx), list(score)
+
+
+def ac_lookup_batch_noalloc(queries, cache, out_idx, out_score=None, stream=None):
+    """ac_lookup_batch on a stream with device outputs and no allocation in the library:
+    queries [nq, dim], cache [n, dim] fp16 CUDA tensors; out_idx int64 [nq] and out_score
+    float32 [nq] (or None) CUDA tensors receive the results."""
+    nq, dim = queries.shape
+    if cache.shape[1] != dim:
+        raise ValueError("ac_lookup_batch_noalloc: query and cache widths differ")
+    _check(lib.ac_lookup_batch_noalloc(_ptr(queries), nq, _ptr(cache), cache.shape[0], dim, _ptr(out_idx),
+                                       _ptr(out_score), _stream(stream)))
 
 
 def ac_fetch_latent(cache_latents, idx, latent, stream=None):
