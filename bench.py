@@ -120,26 +120,47 @@ def device_weights(torch, dn, cfg, seed):
     return blob
 
 
+# Single-GEMM workloads of the 32x32 SD-XL transformer blocks (M = 2048 tokens at batch 2
+# with guidance): name -> (M, N outputs, K, GEGLU, fp32 residual + fp32 output).
+GEMM_CASES = {
+    "ffin": (2048, 5120, 1280, True, False),    # FF-in, 2 x 5120 packed columns -> 5120 GEGLU outputs
+    "proj": (2048, 1280, 1280, False, True),    # attention out-projection into the fp32 residual stream
+    "qkv": (2048, 3840, 1280, False, False),    # fused Q, K, V projection (bf16 output)
+    "ffout": (2048, 1280, 5120, False, True),   # FF-out into the fp32 residual stream
+}
+
+
+def gemm_case(torch, dn, name, stream):
+    """Operands of one GEMM case and a function that launches it once on `stream`."""
+    M, N, K, geglu, resid = GEMM_CASES[name]
+    Nw = 2 * N if geglu else N
+    x = torch.randn((M, K), device="cuda").to(torch.bfloat16)
+    w = (torch.randn((Nw, K), device="cuda") / math.sqrt(K)).to(torch.bfloat16)
+    b = torch.randn(Nw, device="cuda")
+    r = torch.randn((M, N), device="cuda") if resid else None
+    y = torch.empty((M, N), device="cuda", dtype=torch.float32 if resid else torch.bfloat16)
+    w = dn.pack_weight(dn.DN_BF16, w, Nw, K)
+
+    def launch():
+        dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, resid=r, resid_f32=resid, y_f32=resid, geglu=geglu,
+                     stream=stream)
+    return launch, 2.0 * M * Nw * K
+
+
 def roofline_ff_in(torch, dn, stream, iters=20):
     """FF-in GEGLU GEMM of a 32x32 SD-XL transformer block: M = 2048 tokens (batch 2),
     K = 1280, 2 x 5120 packed output columns -> 5120 GEGLU outputs."""
-    M, N, K = 2048, 5120, 1280
-    x = torch.randn((M, K), device="cuda").to(torch.bfloat16)
-    w = (torch.randn((2 * N, K), device="cuda") / math.sqrt(K)).to(torch.bfloat16)
-    b = torch.randn(2 * N, device="cuda")
-    y = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
-    w = dn.pack_weight(dn.DN_BF16, w, 2 * N, K)
+    launch, flops = gemm_case(torch, dn, "ffin", stream)
     for _ in range(3):
-        dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True, stream=stream)
+        launch()
     # one event pair around each launch, on the stream the kernel runs on
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
     for e0, e1 in ev:
         e0.record(stream)
-        dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, geglu=True, stream=stream)
+        launch()
         e1.record(stream)
     torch.cuda.synchronize()
     avg_s = sum(e0.elapsed_time(e1) for e0, e1 in ev) / 1e3 / iters
-    flops = 2.0 * M * (2 * N) * K
     achieved = flops / avg_s / 1e12
     return {"kernel": "gemm_frag_kernel<bf16,128x256> FF-in GEGLU 2048x10240x1280", "bound": "mfma",
             "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -148,11 +169,13 @@ def roofline_ff_in(torch, dn, stream, iters=20):
             "kernel_source_hash": kernel_source_hash()}
 
 
-def profile_kernel(torch, dn):
-    """Counter-collection mode: 20 launches of the FF-in GEMM, then a plain device
-    copy of 256 MiB (its FETCH_SIZE / WRITE_SIZE calibrate the counters)."""
+def profile_kernel(torch, dn, name):
+    """Counter-collection mode: 23 launches of one GEMM case (GEMM_CASES), then a plain
+    device copy of 256 MiB (its FETCH_SIZE / WRITE_SIZE calibrate the counters)."""
     stream = torch.cuda.current_stream()
-    roofline_ff_in(torch, dn, stream)
+    launch, _ = gemm_case(torch, dn, name, stream)
+    for _ in range(23):
+        launch()
     a = torch.empty(64 << 20, device="cuda", dtype=torch.float32).fill_(1.0)
     b = torch.empty_like(a)
     torch.cuda.synchronize()
@@ -369,8 +392,9 @@ def main():
     ap.add_argument("--ac-queries", type=int, default=2,
                     help="queries per k in the approximate-caching sweep (the workload names 64; 2 keeps the "
                          "default run short)")
-    ap.add_argument("--profile-kernel", action="store_true",
-                    help="only launch the FF-in GEMM 20 times and a 256 MiB copy (counter collection)")
+    ap.add_argument("--profile-kernel", nargs="?", const="ffin", default=None, choices=sorted(GEMM_CASES),
+                    help="only launch one GEMM of a 32x32 transformer block 23 times (default: FF-in) and a "
+                         "256 MiB copy (counter collection)")
     ap.add_argument("--lookup-only", action="store_true",
                     help="only the cache lookup (100,000 x 768 fp16, warm and cold): one JSON line")
     ap.add_argument("--sweep-batch", action="store_true",
@@ -388,7 +412,7 @@ def main():
     assert torch.cuda.is_available()
     torch.cuda.set_device(0)
     if args.profile_kernel:
-        profile_kernel(torch, dn)
+        profile_kernel(torch, dn, args.profile_kernel)
         return
     if args.sweep_batch:
         sweep_batch(torch, dn, W, args)

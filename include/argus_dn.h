@@ -16,6 +16,7 @@
  *   dn_denoise_capture                 the same, writing the latent after chosen iterations (cache write)
  *   ac_lookup                          top-1 cosine search over the prompt-embedding cache
  *   ac_lookup_batch                    the same search for many queries in one pass over the cache
+ *   ac_lookup_batch_k                  ac_lookup_batch + the approximation level K chosen from the similarity
  *   ac_lookup_batch_noalloc            ac_lookup_batch on a stream, results in device memory, no allocation
  *   ac_fetch_latent                    copy cached latent #idx into an fp32 latent buffer
  *   dn_unet_eps                        one UNet evaluation + guidance (per-step check hook)
@@ -235,6 +236,30 @@ dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64
  * overlap on one device race on them. */
 dn_status ac_lookup_batch(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n, int32_t dim,
                           int64_t* out_idx, float* out_score);
+
+/* Similarity-driven approximation level (Sec. 2.1: the retrieved prompt's similarity
+ * decides the approximation level K, i.e. how many of the N iterations the cached
+ * state lets the new prompt skip; more similar prompts tolerate a larger K). The
+ * paper gives no rule; the table is an input of the caller (e.g. derived from
+ * offline quality profiles): n_thresholds = L in [0, 15] strictly increasing finite
+ * cosines t_1 < ... < t_L and L + 1 non-decreasing levels K_0 <= ... <= K_L (>= 0).
+ * A retrieved cosine s (the fp32 value reported in out_score) gets K_j with
+ * j = #{i : s >= t_i}; a query that retrieved nothing (index -1) gets K = 0. */
+#define AC_MAX_K_LEVELS 16
+typedef struct {
+  int32_t n_thresholds;
+  float threshold[AC_MAX_K_LEVELS - 1];
+  int32_t level[AC_MAX_K_LEVELS];
+} ac_k_table;
+
+/* ac_lookup_batch that also returns the approximation level of every query
+ * (out_k host int32 [nq]) from `table` (host, read during the call), computed on
+ * the GPU from the same fp32 cosine it reports. The caller then resumes query j
+ * from cached slot K = out_k[j] of row out_idx[j] (dn_denoise with start_step = K).
+ * Synchronous; DN_EINVAL for a malformed table before anything runs. */
+dn_status ac_lookup_batch_k(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n,
+                            int32_t dim, const ac_k_table* table, int64_t* out_idx, float* out_score,
+                            int32_t* out_k);
 
 /* For callers that cannot allocate — code under HIP graph capture, tight serving
  * loops, harnesses that forbid allocation: the search of ac_lookup_batch (same

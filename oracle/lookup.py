@@ -72,3 +72,29 @@ def top1_batch(queries, cache):
         idx[j] = int(np.argmax(s[j]))
         score[j] = float(s[j, idx[j]])
     return idx, score
+
+
+def select_k(scores, thresholds, levels):
+    """Approximation level chosen from the similarity of the retrieved prompt (Sec. 2.1:
+    the cached state to resume from is picked by how similar the cached prompt is; the
+    more similar, the more iterations may be skipped). Reading: a monotone threshold
+    table with thresholds t_1 < ... < t_L and levels K_0 <= ... <= K_L;
+    a retrieved cosine s gets K_j with j = #{i : s >= t_i}, compared in the precision the
+    score is given in (fp32 on both sides). A query that retrieved nothing (index -1,
+    score nan) gets K = 0: there is no cached state to resume from.
+    scores [nq] fp32, thresholds [L], levels [L + 1] -> K [nq] int32."""
+    s = np.asarray(scores, dtype=np.float32)
+    t = np.asarray(thresholds, dtype=np.float32)
+    lv = [int(v) for v in levels]
+    if len(lv) != t.size + 1:
+        raise ValueError("levels must have one entry more than thresholds")
+    out = np.zeros(s.size, np.int32)
+    for q in range(s.size):
+        if np.isnan(s[q]):
+            continue
+        j = 0
+        for i in range(t.size):
+            if s[q] >= t[i]:
+                j = i + 1
+        out[q] = lv[j]
+    return out

@@ -1,6 +1,7 @@
 // C ABI of the denoise-loop library: argument checks, error mapping and the
 // single-kernel entry points. Every entry point catches all C++ exceptions.
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -70,13 +71,14 @@ hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 struct LookupRes {
   long long idx;
   float score;
+  int k;
 };
 struct LookupWs {
   std::mutex mu;
   std::vector<void*> ws;
   std::vector<LookupRes*> res;
   std::vector<void*> batch_ws;        // per-workgroup winners of the batched scan
-  std::vector<long long*> batch_res;  // pinned: 64 indices, then 64 scores
+  std::vector<long long*> batch_res;  // pinned: 64 indices, then 64 scores, then 64 levels
 };
 LookupWs g_lookup;
 
@@ -92,7 +94,7 @@ void lookup_state(int dev, void** ws, LookupRes** res) {
   *res = g_lookup.res[dev];
 }
 
-void lookup_batch_state(int dev, void** ws, long long** idx, float** score) {
+void lookup_batch_state(int dev, void** ws, long long** idx, float** score, int** lev) {
   std::lock_guard<std::mutex> lk(g_lookup.mu);
   if ((int)g_lookup.batch_ws.size() <= dev) {
     g_lookup.batch_ws.resize(dev + 1, nullptr);
@@ -101,10 +103,83 @@ void lookup_batch_state(int dev, void** ws, long long** idx, float** score) {
   const int mq = dn::lookup_batch_max_queries();
   if (!g_lookup.batch_ws[dev]) DN_HIP(hipMalloc(&g_lookup.batch_ws[dev], dn::lookup_batch_workspace_bytes()));
   if (!g_lookup.batch_res[dev])
-    DN_HIP(hipHostMalloc(reinterpret_cast<void**>(&g_lookup.batch_res[dev]), mq * (sizeof(long long) + sizeof(float))));
+    DN_HIP(hipHostMalloc(reinterpret_cast<void**>(&g_lookup.batch_res[dev]),
+                         mq * (sizeof(long long) + sizeof(float) + sizeof(int))));
   *ws = g_lookup.batch_ws[dev];
   *idx = g_lookup.batch_res[dev];
   *score = reinterpret_cast<float*>(g_lookup.batch_res[dev] + mq);
+  *lev = reinterpret_cast<int*>(*score + mq);
+}
+
+// Checks a similarity-to-level table and converts it for the kernels.
+dn::KTable k_table(const ac_k_table* t) {
+  DN_CHECK(t, "ac_k_table: null table");
+  DN_CHECK(t->n_thresholds >= 0 && t->n_thresholds < AC_MAX_K_LEVELS,
+           "ac_k_table: n_thresholds must be in [0, " + std::to_string(AC_MAX_K_LEVELS - 1) + "]");
+  dn::KTable k;
+  k.n = t->n_thresholds;
+  for (int i = 0; i < k.n; ++i) {
+    DN_CHECK(std::isfinite(t->threshold[i]), "ac_k_table: thresholds must be finite");
+    DN_CHECK(i == 0 || t->threshold[i] > t->threshold[i - 1], "ac_k_table: thresholds must increase strictly");
+    k.thr[i] = t->threshold[i];
+  }
+  for (int j = 0; j <= k.n; ++j) {
+    DN_CHECK(t->level[j] >= 0, "ac_k_table: levels must be >= 0");
+    DN_CHECK(j == 0 || t->level[j] >= t->level[j - 1], "ac_k_table: levels must not decrease");
+    k.level[j] = t->level[j];
+  }
+  return k;
+}
+
+// The batched search of ac_lookup_batch / ac_lookup_batch_k (host results; level per
+// query when kt is given).
+void lookup_batch_host(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n, int32_t dim,
+                       int64_t* out_idx, float* out_score, const dn::KTable* kt, int32_t* out_k, const char* who) {
+  const std::string w(who);
+  DN_CHECK(query_embs && cache_embs && out_idx, w + ": null pointer");
+  DN_CHECK(nq >= 1, w + ": nq must be >= 1");
+  DN_CHECK(n >= 1, w + ": n must be >= 1");
+  DN_CHECK(dim >= 1, w + ": dim must be >= 1");
+  DN_CHECK(!kt || out_k, w + ": null level output");
+  int dev = 0;
+  DN_HIP(hipGetDevice(&dev));
+  if (!dn::lookup_batch_supported(query_embs, cache_embs, n, dim)) {
+    // other widths or alignments: one scan per query
+    void* ws = nullptr;
+    LookupRes* res = nullptr;
+    lookup_state(dev, &ws, &res);
+    for (int j = 0; j < nq; ++j) {
+      res->idx = -1;
+      res->score = 0.f;
+      res->k = -1;
+      dn::lookup(query_embs + (size_t)j * dim, cache_embs, n, dim, ws, &res->idx, &res->score, nullptr, kt,
+                 &res->k);
+      DN_HIP(hipStreamSynchronize(nullptr));
+      out_idx[j] = *static_cast<volatile long long*>(&res->idx);
+      if (out_score) out_score[j] = *static_cast<volatile float*>(&res->score);
+      if (kt) out_k[j] = *static_cast<volatile int*>(&res->k);
+    }
+    return;
+  }
+  void* ws = nullptr;
+  long long* ridx = nullptr;
+  float* rscore = nullptr;
+  int* rk = nullptr;
+  lookup_batch_state(dev, &ws, &ridx, &rscore, &rk);
+  const int mq = dn::lookup_batch_max_queries();
+  for (int j0 = 0; j0 < nq; j0 += mq) {
+    const int m = nq - j0 < mq ? nq - j0 : mq;
+    for (int j = 0; j < m; ++j) ridx[j] = -2;
+    dn::lookup_batch(query_embs + (size_t)j0 * dim, m, cache_embs, n, dim, ws, ridx, rscore, nullptr, kt, rk);
+    DN_HIP(hipStreamSynchronize(nullptr));
+    for (int j = 0; j < m; ++j) {
+      const long long idx = static_cast<volatile long long*>(ridx)[j];
+      DN_CHECK(idx >= -1 && idx < n, w + ": result not written");
+      out_idx[j0 + j] = idx;
+      if (out_score) out_score[j0 + j] = static_cast<volatile float*>(rscore)[j];
+      if (kt) out_k[j0 + j] = static_cast<volatile int*>(rk)[j];
+    }
+  }
 }
 
 bool is_dtype(int32_t d) { return d == DN_FP32 || d == DN_BF16; }
@@ -268,44 +343,16 @@ dn_status ac_lookup(const uint16_t* query_emb, const uint16_t* cache_embs, int64
 dn_status ac_lookup_batch(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n, int32_t dim,
                           int64_t* out_idx, float* out_score) {
   return guarded([&] {
-    DN_CHECK(query_embs && cache_embs && out_idx, "ac_lookup_batch: null pointer");
-    DN_CHECK(nq >= 1, "ac_lookup_batch: nq must be >= 1");
-    DN_CHECK(n >= 1, "ac_lookup_batch: n must be >= 1");
-    DN_CHECK(dim >= 1, "ac_lookup_batch: dim must be >= 1");
-    int dev = 0;
-    DN_HIP(hipGetDevice(&dev));
-    if (!dn::lookup_batch_supported(query_embs, cache_embs, n, dim)) {
-      // other widths or alignments: one scan per query
-      void* ws = nullptr;
-      LookupRes* res = nullptr;
-      lookup_state(dev, &ws, &res);
-      for (int j = 0; j < nq; ++j) {
-        res->idx = -1;
-        res->score = 0.f;
-        dn::lookup(query_embs + (size_t)j * dim, cache_embs, n, dim, ws, &res->idx, &res->score, nullptr);
-        DN_HIP(hipStreamSynchronize(nullptr));
-        out_idx[j] = *static_cast<volatile long long*>(&res->idx);
-        if (out_score) out_score[j] = *static_cast<volatile float*>(&res->score);
-      }
-      return;
-    }
-    void* ws = nullptr;
-    long long* ridx = nullptr;
-    float* rscore = nullptr;
-    lookup_batch_state(dev, &ws, &ridx, &rscore);
-    const int mq = dn::lookup_batch_max_queries();
-    for (int j0 = 0; j0 < nq; j0 += mq) {
-      const int m = nq - j0 < mq ? nq - j0 : mq;
-      for (int j = 0; j < m; ++j) ridx[j] = -2;
-      dn::lookup_batch(query_embs + (size_t)j0 * dim, m, cache_embs, n, dim, ws, ridx, rscore, nullptr);
-      DN_HIP(hipStreamSynchronize(nullptr));
-      for (int j = 0; j < m; ++j) {
-        const long long idx = static_cast<volatile long long*>(ridx)[j];
-        DN_CHECK(idx >= -1 && idx < n, "ac_lookup_batch: result not written");
-        out_idx[j0 + j] = idx;
-        if (out_score) out_score[j0 + j] = static_cast<volatile float*>(rscore)[j];
-      }
-    }
+    lookup_batch_host(query_embs, nq, cache_embs, n, dim, out_idx, out_score, nullptr, nullptr, "ac_lookup_batch");
+  });
+}
+
+dn_status ac_lookup_batch_k(const uint16_t* query_embs, int32_t nq, const uint16_t* cache_embs, int64_t n,
+                            int32_t dim, const ac_k_table* table, int64_t* out_idx, float* out_score,
+                            int32_t* out_k) {
+  return guarded([&] {
+    const dn::KTable kt = k_table(table);
+    lookup_batch_host(query_embs, nq, cache_embs, n, dim, out_idx, out_score, &kt, out_k, "ac_lookup_batch_k");
   });
 }
 

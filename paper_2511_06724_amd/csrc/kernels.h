@@ -161,12 +161,21 @@ template <typename T> void pack(const PackParams& p, hipStream_t s);
 void pack_bias(float* dst, int n, const float* src, int src_n, int row_mode, int D, int Dp, hipStream_t s);
 
 // ---------------------------------------------------------------- cache lookup
+// Similarity-driven approximation level: a retrieved cosine s gets level[j],
+// j = #{i < n : s >= thr[i]} (fp32 comparisons); a query that retrieved nothing gets 0.
+constexpr int kMaxKLevels = 16;
+struct KTable {
+  int n = 0;
+  float thr[kMaxKLevels - 1] = {};
+  int level[kMaxKLevels] = {};
+};
 // Top-1 cosine row of cache [n][dim] (fp16) for q [dim]: writes the index (-1 when no
 // row has a defined cosine) and the cosine to idx_out / score_out, which may be device
 // memory or pinned host memory. ws: lookup_workspace_bytes() of device memory.
 size_t lookup_workspace_bytes();
+// With k_out != nullptr the reduction also writes the level of kt for the result.
 void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_out,
-            float* score_out, hipStream_t s);
+            float* score_out, hipStream_t s, const KTable* kt = nullptr, int* k_out = nullptr);
 // Top-1 rows of cache [n][dim] for nq <= lookup_batch_max_queries() queries q [nq][dim]
 // in one pass over the table (matrix-core scores). idx_out / score_out [nq] (device or
 // pinned host memory); idx -1 for a query with no defined cosine. Needs
@@ -175,6 +184,7 @@ size_t lookup_batch_workspace_bytes();
 int lookup_batch_max_queries();
 bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, long long n, int dim);
 void lookup_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n, int dim, void* ws,
-                  long long* idx_out, float* score_out, hipStream_t s);
+                  long long* idx_out, float* score_out, hipStream_t s, const KTable* kt = nullptr,
+                  int* k_out = nullptr);
 
 }  // namespace dn

@@ -168,12 +168,21 @@ __global__ __launch_bounds__(256) void scan_scalar_kernel(const uint16_t* q, con
   }
 }
 
+// Level of the table for a result (index -1: nothing retrieved, level 0).
+__device__ __forceinline__ int select_level(const KTable& kt, long long idx, float score) {
+  if (idx < 0) return 0;
+  int j = 0;
+  for (int i = 0; i < kt.n; ++i)
+    if (score >= kt.thr[i]) j = i + 1;
+  return kt.level[j];
+}
+
 // Pass 2, one workgroup: every thread loads its (up to kScanBlocks / 256) winners
 // before comparing them; waves reduce with shuffles, then the 4 wave winners in order.
 // The squared norm of q (for the reported cosine) is summed alongside. The result may
 // be written to pinned host memory.
 __global__ __launch_bounds__(256) void reduce_kernel(const Cand* part, int nb, const uint16_t* q, int dim,
-                                                     long long* idx, float* score) {
+                                                     long long* idx, float* score, KTable kt, int* kout) {
   constexpr int kPer = kScanBlocks / 256;
   __shared__ float ws_s[4], ws_q[4];
   __shared__ long long ws_i[4];
@@ -223,8 +232,11 @@ __global__ __launch_bounds__(256) void reduce_kernel(const Cand* part, int nb, c
       qn += ws_q[k];
     }
     // A zero query (or a cache of zero rows) has no defined cosine: report no row.
-    *idx = (qn > 0.f && bs > -INFINITY) ? bi : -1;
-    *score = bs * rsqrtf(qn);
+    const long long r = (qn > 0.f && bs > -INFINITY) ? bi : -1;
+    const float sc = bs * rsqrtf(qn);
+    *idx = r;
+    *score = sc;
+    if (kout) *kout = select_level(kt, r, sc);
   }
 }
 
@@ -369,7 +381,7 @@ __global__ __launch_bounds__(BatchCfg<KS>::kWaves * 64) void scan_mfma_kernel(co
 // One workgroup per query: the nb workgroup winners of its column, and |q|^2 for the
 // reported cosine. Writes idx[j] = -1 where the query has no defined cosine.
 __global__ __launch_bounds__(256) void reduce_batch_kernel(const Cand* part, int nb, const uint16_t* q, int dim,
-                                                           long long* idx, float* score) {
+                                                           long long* idx, float* score, KTable kt, int* kout) {
   __shared__ float ws_s[4], ws_q[4];
   __shared__ long long ws_i[4];
   const int j = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
@@ -406,8 +418,11 @@ __global__ __launch_bounds__(256) void reduce_batch_kernel(const Cand* part, int
       }
       qn += ws_q[k];
     }
-    idx[j] = (qn > 0.f && bs > -INFINITY) ? bi : -1;
-    score[j] = bs * rsqrtf(qn);
+    const long long r = (qn > 0.f && bs > -INFINITY) ? bi : -1;
+    const float sc = bs * rsqrtf(qn);
+    idx[j] = r;
+    score[j] = sc;
+    if (kout) kout[j] = select_level(kt, r, sc);
   }
 }
 
@@ -433,7 +448,7 @@ int launch_batch(const uint16_t* q, int nq, const uint16_t* cache, int n, Cand* 
 size_t lookup_workspace_bytes() { return sizeof(Cand) * kScanBlocks; }
 
 void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void* ws, long long* idx_out,
-            float* score_out, hipStream_t s) {
+            float* score_out, hipStream_t s, const KTable* kt, int* k_out) {
   DN_CHECK(n >= 1 && dim >= 1, "lookup: empty cache");
   Cand* part = static_cast<Cand*>(ws);
   const long long want = (n + 15) / 16;
@@ -454,7 +469,9 @@ void lookup(const uint16_t* q, const uint16_t* cache, long long n, int dim, void
     DN_CHECK(dim <= 16384, "lookup: dim too large for the scalar path");
     hipLaunchKernelGGL(scan_scalar_kernel, dim3(nb), dim3(256), dim * sizeof(float), s, q, cache, n, dim, part);
   }
-  hipLaunchKernelGGL(reduce_kernel, dim3(1), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out);
+  const KTable tab = kt ? *kt : KTable();
+  hipLaunchKernelGGL(reduce_kernel, dim3(1), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out, tab,
+                     kt ? k_out : nullptr);
   DN_HIP(hipGetLastError());
 }
 
@@ -473,7 +490,7 @@ bool lookup_batch_supported(const uint16_t* q, const uint16_t* cache, long long 
 }
 
 void lookup_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n, int dim, void* ws,
-                  long long* idx_out, float* score_out, hipStream_t s) {
+                  long long* idx_out, float* score_out, hipStream_t s, const KTable* kt, int* k_out) {
   DN_CHECK(n >= 1 && dim >= 1, "lookup_batch: empty cache");
   DN_CHECK(nq >= 1 && nq <= kBatchQ, "lookup_batch: 1 to 64 queries per pass");
   DN_CHECK(lookup_batch_supported(q, cache, n, dim),
@@ -487,7 +504,9 @@ void lookup_batch(const uint16_t* q, int nq, const uint16_t* cache, long long n,
     case 768: nb = launch_batch<24>(q, nq, cache, n32, part, s); break;
     default: nb = launch_batch<32>(q, nq, cache, n32, part, s); break;
   }
-  hipLaunchKernelGGL(reduce_batch_kernel, dim3(nq), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out);
+  const KTable tab = kt ? *kt : KTable();
+  hipLaunchKernelGGL(reduce_batch_kernel, dim3(nq), dim3(256), 0, s, part, nb, q, dim, idx_out, score_out, tab,
+                     kt ? k_out : nullptr);
   DN_HIP(hipGetLastError());
 }
 

@@ -22,9 +22,17 @@ ABI_VERSION = 1
 MAX_LEVELS = 4
 
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_denoise_capture", "dn_unet_eps", "ac_lookup",
-            "ac_lookup_batch", "ac_lookup_batch_noalloc", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
+            "ac_lookup_batch", "ac_lookup_batch_k", "ac_lookup_batch_noalloc", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
             "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_layernorm_slabs", "dn_op_linear_vt",
             "dn_destroy", "dn_last_error")
+
+
+AC_MAX_K_LEVELS = 16
+
+
+class _KTable(C.Structure):
+    _fields_ = [("n_thresholds", C.c_int32), ("threshold", C.c_float * (AC_MAX_K_LEVELS - 1)),
+                ("level", C.c_int32 * AC_MAX_K_LEVELS)]
 
 
 class DnError(RuntimeError):
@@ -69,6 +77,7 @@ def _load():
         "dn_unet_eps": [P, P, I32, P, F32, P, P, P],
         "ac_lookup": [P, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
         "ac_lookup_batch": [P, I32, P, I64, I32, C.POINTER(I64), C.POINTER(F32)],
+        "ac_lookup_batch_k": [P, I32, P, I64, I32, C.POINTER(_KTable), P, P, P],
         "ac_lookup_batch_noalloc": [P, I32, P, I64, I32, P, P, P],
         "ac_fetch_latent": [P, I64, I64, I64, P, P],
         "dn_packed_weight_elems": [I32, I32, I32, C.POINTER(I64)],
@@ -229,6 +238,34 @@ def ac_lookup_batch(queries, cache):
     score = (C.c_float * nq)()
     _check(lib.ac_lookup_batch(_ptr(queries), nq, _ptr(cache), n, dim, idx, score))
     return list(idx), list(score)
+
+
+def k_table(thresholds, levels):
+    """ac_k_table from thresholds [L] and levels [L + 1] (no checks: the library checks)."""
+    t = _KTable()
+    t.n_thresholds = len(thresholds)
+    for i, v in enumerate(thresholds):
+        t.threshold[i] = v
+    for i, v in enumerate(levels):
+        t.level[i] = v
+    return t
+
+
+def ac_lookup_batch_k(queries, cache, thresholds, levels):
+    """(indices, cosines, levels K) for every query: ac_lookup_batch plus the approximation
+    level chosen from the retrieved cosine by the threshold table (thresholds [L],
+    levels [L + 1])."""
+    nq, dim = queries.shape
+    if cache.shape[1] != dim:
+        raise ValueError("ac_lookup_batch_k: query and cache widths differ")
+    if len(thresholds) >= AC_MAX_K_LEVELS or len(levels) > AC_MAX_K_LEVELS:
+        raise ValueError("ac_lookup_batch_k: at most 15 thresholds")
+    idx = (C.c_int64 * nq)()
+    score = (C.c_float * nq)()
+    k = (C.c_int32 * nq)()
+    tab = k_table(thresholds, levels)
+    _check(lib.ac_lookup_batch_k(_ptr(queries), nq, _ptr(cache), cache.shape[0], dim, C.byref(tab), idx, score, k))
+    return list(idx), list(score), list(k)
 
 
 def ac_lookup_batch_noalloc(queries, cache, out_idx, out_score=None, stream=None):

@@ -154,3 +154,53 @@ def test_batch_duplicates_give_lowest_index_and_errors_touch_nothing():
     assert dn.lib.ac_lookup_batch(None, 2, 1, 5, 768, out, None) == dn.DN_EINVAL
     assert dn.lib.ac_lookup_batch(1, 0, 1, 5, 768, out, None) == dn.DN_EINVAL
     assert list(out) == [-7, -7]
+
+
+# ----------------------------------------------------------------------------- similarity-driven K
+
+K_THR = [0.80, 0.85, 0.90, 0.93]
+K_LEV = [0, 5, 10, 15, 25]
+
+
+@pytest.mark.parametrize("n,dim,nq", [(100_000, 768, 70), (5000, 77, 9)])
+def test_lookup_batch_k_matches_oracle_levels(n, dim, nq):
+    """ac_lookup_batch_k: indices and cosines bitwise those of ac_lookup_batch; the level
+    of each query bit-exactly the oracle's select_k on the reported fp32 cosine, and the
+    oracle's select_k on its own fp64 cosine (rounded to fp32) except within 1e-6 of a
+    threshold; a zero query gets index -1 and K = 0. dim 77 runs the per-query scan."""
+    announce(f"lookup batch + K: n={n} dim={dim} nq={nq}")
+    cache = W.cache_embeddings(n, dim, seed=7)
+    qs, rows = W.planted_queries(cache, nq, seed=9, cos_lo=0.75, cos_hi=0.97)
+    qs[3] = 0
+    cd = torch.from_numpy(cache.view(np.uint16)).to(DEV)
+    qd = torch.from_numpy(qs.view(np.uint16).copy()).to(DEV)
+    idx, score, k = dn.ac_lookup_batch_k(qd, cd, K_THR, K_LEV)
+    bidx, bscore = dn.ac_lookup_batch(qd, cd)
+    assert idx == bidx
+    assert np.array_equal(np.asarray(score, np.float32).view(np.uint32), np.asarray(bscore, np.float32).view(np.uint32))
+    assert idx[3] == -1 and k[3] == 0
+    assert list(OL.select_k(np.asarray(score, np.float32), K_THR, K_LEV)) == k
+    ridx, rscore = OL.top1_batch(qs, cache)
+    rk = OL.select_k(rscore.astype(np.float32), K_THR, K_LEV)
+    for j in range(nq):
+        if j == 3:
+            continue
+        assert idx[j] == rows[j]
+        if rk[j] != k[j]:
+            assert min(abs(rscore[j] - t) for t in K_THR) < 1e-6, (j, rscore[j], k[j], rk[j])
+    assert len(set(k)) >= 3   # the planted cosines span several levels
+
+
+def test_lookup_batch_k_rejects_bad_tables():
+    announce("lookup batch + K: table errors")
+    cache = torch.from_numpy(W.cache_embeddings(256, 256, seed=1).view(np.uint16)).to(DEV)
+    q = cache[:2].clone()
+    for thr, lev in (([0.9, 0.8], [0, 5, 10]), ([0.8, float("nan")], [0, 5, 10]), ([0.8], [5, 0]),
+                     ([0.8], [-1, 5]), ([0.1 * i for i in range(15)] + [2.0], list(range(17)))):
+        t = dn.k_table(thr[:15], lev[:16])
+        t.n_thresholds = len(thr)
+        idx = (dn.C.c_int64 * 2)(-7, -7)
+        kk = (dn.C.c_int32 * 2)(-7, -7)
+        code = dn.lib.ac_lookup_batch_k(q.data_ptr(), 2, cache.data_ptr(), 256, 256, dn.C.byref(t), idx, None, kk)
+        assert code == dn.DN_EINVAL, (thr, lev)
+        assert list(idx) == [-7, -7] and list(kk) == [-7, -7]
