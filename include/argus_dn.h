@@ -22,6 +22,7 @@
  *   dn_unet_eps                        one UNet evaluation + guidance (per-step check hook)
  *   dn_op_*                            single-kernel entry points (kernel checks, timing)
  *   dn_destroy, dn_last_error
+ *   argus_oda, argus_route, argus_select_worker   routing control plane on the host (Sec. 4.3-4.4)
  *
  * Conventions (every call):
  *   - Pointers marked "device" are HIP device allocations owned by the caller;
@@ -386,6 +387,41 @@ dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int
 dn_status dn_op_layernorm_slabs(int32_t dtype, float* x, void* y, int64_t M, int32_t C, const float* gamma,
                                 const float* beta, float eps, const float* slabs, int32_t nsplit, const float* bias,
                                 int32_t resid, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Routing control plane (host only, no GPU work; Sec. 4.3-4.4). Approximation levels
+ * are indexed 0 .. n-1 from the slowest / most accurate to the fastest / most
+ * approximate (for approximate caching: increasing K). All arrays are host memory
+ * read or written during the call. These calls report errors through
+ * argus_last_error(), not dn_last_error().
+ * ------------------------------------------------------------------------- */
+#define ARGUS_MAX_LEVELS 64
+
+/* Optimized Distribution Aligner (Sec. 4.3, Alg. 1): from the classifier's demand
+ * histogram H[n] (share of prompts whose optimal level is i) and the solver's load
+ * split F[n] (share of the load each level serves; sum F = sum H > 0, both
+ * non-negative), writes the Probabilistic Approximation Shift Map pasm[n][n]
+ * (row-major): pasm[i][j] = probability that a prompt whose optimal level is i is
+ * served at level j. Levels are visited from the fastest to the slowest: excess
+ * demand moves to the next slower level (proportionally for all prompts present
+ * there), a shortfall is filled from the nearest slower levels first. Every row sums
+ * to 1 and sum_i H[i] pasm[i][j] = F[j]. A row with H[i] = 0 is the identity. */
+dn_status argus_oda(const double* H, const double* F, int32_t n, double* pasm);
+
+/* Prompt Scheduler (Sec. 4.4): the level a prompt whose optimal level is `level` is
+ * sent to, drawn from PASM row `level` with a uniform number u in [0, 1) supplied by
+ * the caller: the first j whose cumulative probability (from level 0) exceeds u, or
+ * the last level of positive probability if rounding leaves the row sum <= u. */
+dn_status argus_route(const double* pasm, int32_t n, int32_t level, double u, int32_t* out_level);
+
+/* Worker selector, Eq. 3 (Sec. 4.4): among the n_workers workers whose
+ * worker_level[w] equals `level`, the one minimising queue_len[w] * t_proc[w] (queued
+ * requests times its generation time at that level), lowest w on ties; *out_worker =
+ * -1 when no worker runs the level. */
+dn_status argus_select_worker(const int32_t* queue_len, const double* t_proc, const int32_t* worker_level,
+                              int32_t n_workers, int32_t level, int32_t* out_worker);
+
+const char* argus_last_error(void); /* message of the calling thread's last control-plane error */
 
 void dn_destroy(dn_handle* h); /* NULL-safe; synchronizes the device first */
 

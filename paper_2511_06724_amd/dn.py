@@ -24,7 +24,7 @@ MAX_LEVELS = 4
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_denoise_capture", "dn_unet_eps", "ac_lookup",
             "ac_lookup_batch", "ac_lookup_batch_k", "ac_lookup_batch_noalloc", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
             "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_layernorm_slabs", "dn_op_linear_vt",
-            "dn_destroy", "dn_last_error")
+            "dn_destroy", "dn_last_error", "argus_oda", "argus_route", "argus_select_worker", "argus_last_error")
 
 
 AC_MAX_K_LEVELS = 16
@@ -89,6 +89,10 @@ def _load():
         "dn_op_groupnorm": [I32, P, P, I32, I32, I32, I32, P, P, F32, I32, P],
         "dn_op_layernorm": [I32, P, P, I64, I32, P, P, F32, P],
         "dn_op_layernorm_slabs": [I32, P, P, I64, I32, P, P, F32, P, I32, P, I32, P],
+        "argus_oda": [P, P, I32, P],
+        "argus_route": [P, I32, I32, C.c_double, C.POINTER(I32)],
+        "argus_select_worker": [P, P, P, I32, I32, C.POINTER(I32)],
+        "argus_last_error": [],
         "dn_destroy": [P],
         "dn_last_error": [],
     }
@@ -98,6 +102,7 @@ def _load():
         f.restype = C.c_int
     lib.dn_destroy.restype = None
     lib.dn_last_error.restype = C.c_char_p
+    lib.argus_last_error.restype = C.c_char_p
     return lib
 
 
@@ -332,3 +337,37 @@ def op_layernorm(dtype, x, y, M, Cc, gamma, beta, eps, stream=None):
 def op_layernorm_slabs(dtype, x, y, M, Cc, gamma, beta, eps, slabs, nsplit, bias=None, resid=True, stream=None):
     _check(lib.dn_op_layernorm_slabs(dtype, _ptr(x), _ptr(y), M, Cc, _ptr(gamma), _ptr(beta), eps, _ptr(slabs), nsplit,
                                      _ptr(bias), int(resid), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------- routing control plane (host)
+
+def _check_ctl(code):
+    if code != DN_OK:
+        raise DnError(code, lib.argus_last_error().decode())
+
+
+def oda(H, F):
+    """PASM [n, n] (numpy fp64) from the demand histogram H and the load split F."""
+    H = np.ascontiguousarray(H, dtype=np.float64)
+    F = np.ascontiguousarray(F, dtype=np.float64)
+    if H.shape != F.shape or H.ndim != 1:
+        raise ValueError("oda: H and F must be 1-D of the same length")
+    out = np.zeros((H.size, H.size), np.float64)
+    _check_ctl(lib.argus_oda(H.ctypes.data, F.ctypes.data, H.size, out.ctypes.data))
+    return out
+
+
+def route(pasm, level, u):
+    pasm = np.ascontiguousarray(pasm, dtype=np.float64)
+    out = C.c_int32()
+    _check_ctl(lib.argus_route(pasm.ctypes.data, pasm.shape[0], level, u, C.byref(out)))
+    return out.value
+
+
+def select_worker(queue_len, t_proc, worker_level, level):
+    q = np.ascontiguousarray(queue_len, dtype=np.int32)
+    t = np.ascontiguousarray(t_proc, dtype=np.float64)
+    lv = np.ascontiguousarray(worker_level, dtype=np.int32)
+    out = C.c_int32()
+    _check_ctl(lib.argus_select_worker(q.ctypes.data, t.ctypes.data, lv.ctypes.data, q.size, level, C.byref(out)))
+    return out.value
