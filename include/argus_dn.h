@@ -20,6 +20,7 @@
  *   ac_lookup_batch_noalloc            ac_lookup_batch on a stream, results in device memory, no allocation
  *   ac_fetch_latent                    copy cached latent #idx into an fp32 latent buffer
  *   dn_unet_eps                        one UNet evaluation + guidance (per-step check hook)
+ *   dn_vae_*                           the latent decoder after the loop (Table 3's VAE Decoder)
  *   dn_op_*                            single-kernel entry points (kernel checks, timing)
  *   dn_destroy, dn_last_error
  *   argus_oda, argus_route, argus_select_worker   routing control plane on the host (Sec. 4.3-4.4)
@@ -387,6 +388,67 @@ dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int
 dn_status dn_op_layernorm_slabs(int32_t dtype, float* x, void* y, int64_t M, int32_t C, const float* gamma,
                                 const float* beta, float eps, const float* slabs, int32_t nsplit, const float* bias,
                                 int32_t resid, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Latent decoder: the VAE Decoder of Table 3 (0.050 B parameters, 2481 GFLOP for a
+ * 512 x 512 image), run once per image after the denoise loop to turn the final
+ * latent into the RGB image. KL-autoencoder decoder of latent diffusion:
+ *   z / scaling_factor -> 1x1 conv (latent_c -> latent_c) -> conv3x3 (-> C_top)
+ *   -> ResBlock, single-head self-attention over all positions, ResBlock (at C_top)
+ *   -> up levels l = n_levels-1 .. 0: (layers_per_block + 1) ResBlocks at width
+ *      channels[l] (a 1x1 skip conv where the width changes), then for l > 0 a
+ *      nearest-x2 upsample followed by conv3x3
+ *   -> GroupNorm, SiLU, conv3x3 (channels[0] -> out_c).
+ * ResBlock(x) = skip(x) + conv2(SiLU(GN2(conv1(SiLU(GN1(x)))))) (no time input);
+ * every GroupNorm has gn_groups groups and epsilon gn_eps; the attention's q, k, v and
+ * output projections are linear layers with bias, softmax scale 1/sqrt(C_top).
+ * ------------------------------------------------------------------------- */
+typedef struct dn_vae dn_vae; /* opaque: packed device weights + workspace of one decoder */
+
+/* dtype as in dn_config; batch images; latent_c (<= 64), latent_h x latent_w
+ * (a multiple of 64 positions, at most 65536); n_levels (1..4) widths channels[]
+ * (multiples of 64, <= 2048, divisible by gn_groups), slowest resolution last; the
+ * image is 2^(n_levels-1) times the latent in each direction (at most 4 M pixels). */
+typedef struct {
+  int32_t abi_version; /* must be DN_ABI_VERSION */
+  int32_t dtype;
+  int32_t batch;
+  int32_t latent_c, latent_h, latent_w;
+  int32_t n_levels;
+  int32_t channels[DN_MAX_LEVELS];
+  int32_t layers_per_block;
+  int32_t gn_groups;
+  float gn_eps;
+  float scaling_factor;
+  int32_t out_c;
+} dn_vae_config;
+
+/* Canonical fp32 blob of a decoder (PyTorch layouts, conv [Cout][Cin][kh][kw],
+ * linear [out][in]): post_quant.w [latent_c][latent_c][1][1], .b; conv_in.w, .b;
+ * mid.res0; mid.attn: gn scale, shift, q.w [C][C], q.b, k.w, k.b, v.w, v.b, o.w, o.b;
+ * mid.res1; up levels l = n_levels-1 .. 0: (layers_per_block + 1) ResBlocks, then
+ * (l > 0) up.w [C_l][C_l][3][3], up.b; out GroupNorm scale, shift; conv_out.w, .b.
+ * ResBlock(Cin -> Cout): gn1 scale, shift [Cin]; conv1.w, .b; gn2 scale, shift
+ * [Cout]; conv2.w, .b; if Cin != Cout skip.w [Cout][Cin][1][1], skip.b.
+ * dn_vae_weight_table describes it tensor by tensor as dn_weight_table does. */
+dn_status dn_vae_weight_count(const dn_vae_config* cfg, size_t* n_floats);
+dn_status dn_vae_weight_table(const dn_vae_config* cfg, int64_t* numel, int32_t* fan_in, int32_t* kind,
+                              size_t capacity, size_t* n_tensors);
+
+/* Builds a decoder: validates cfg, copies and packs the blob (host or device memory
+ * per weights_location; the caller keeps it) in the configured dtype and allocates
+ * the workspace of one decode (for a 128 x 128 latent about 4 GB in bf16, including
+ * the 16384 x 16384 fp32 attention scores). Synchronous. DN_EUNSUPPORTED when the
+ * current device is not gfx950. */
+dn_status dn_vae_create(const dn_vae_config* cfg, const float* weights, size_t n_floats, int32_t weights_location,
+                        dn_vae** out);
+
+/* Decodes latent (device fp32 [batch][latent_c][H][W], e.g. the latent dn_denoise
+ * leaves) into image (device fp32 [batch][out_c][H'][W'], H' = 2^(n_levels-1) H).
+ * Asynchronous on `stream`; one decoder serves one stream at a time. */
+dn_status dn_vae_decode(dn_vae* v, const float* latent, float* image, void* stream);
+
+void dn_vae_destroy(dn_vae* v); /* NULL-safe; synchronizes the device first */
 
 /* ---------------------------------------------------------------------------
  * Routing control plane (host only, no GPU work; Sec. 4.3-4.4). Approximation levels

@@ -247,6 +247,9 @@ template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
 struct dn_handle {
   dn::Model* m = nullptr;
 };
+struct dn_vae {
+  dn::Vae* v = nullptr;
+};
 
 extern "C" {
 
@@ -636,6 +639,57 @@ dn_status dn_op_layernorm_slabs(int32_t dtype, float* x, void* y, int64_t M, int
       dn::layernorm_reduce<float>(x, static_cast<float*>(y), M, C, gamma, beta, eps, slabs, nsplit, bias,
                                   resid != 0, as_stream(stream));
   });
+}
+
+dn_status dn_vae_weight_count(const dn_vae_config* cfg, size_t* n_floats) {
+  return guarded([&] {
+    DN_CHECK(cfg && n_floats, "dn_vae_weight_count: null pointer");
+    const auto t = dn::vae_weight_table(*cfg);
+    *n_floats = static_cast<size_t>(t.back().offset + t.back().numel);
+  });
+}
+
+dn_status dn_vae_weight_table(const dn_vae_config* cfg, int64_t* numel, int32_t* fan_in, int32_t* kind,
+                              size_t capacity, size_t* n_tensors) {
+  return guarded([&] {
+    DN_CHECK(cfg && n_tensors, "dn_vae_weight_table: null pointer");
+    const auto t = dn::vae_weight_table(*cfg);
+    DN_CHECK(capacity == 0 || capacity >= t.size(), "dn_vae_weight_table: capacity too small");
+    DN_CHECK(capacity == 0 || (numel && fan_in && kind), "dn_vae_weight_table: null output array");
+    if (capacity)
+      for (size_t i = 0; i < t.size(); ++i) {
+        numel[i] = t[i].numel;
+        fan_in[i] = t[i].fan_in;
+        kind[i] = t[i].kind;
+      }
+    *n_tensors = t.size();
+  });
+}
+
+dn_status dn_vae_create(const dn_vae_config* cfg, const float* weights, size_t n_floats, int32_t weights_location,
+                        dn_vae** out) {
+  return guarded([&] {
+    DN_CHECK(cfg && weights && out, "dn_vae_create: null pointer");
+    DN_CHECK(weights_location == DN_WEIGHTS_HOST || weights_location == DN_WEIGHTS_DEVICE,
+             "dn_vae_create: bad weights_location");
+    dn::Vae* v = dn::vae_create(*cfg, weights, n_floats, weights_location == DN_WEIGHTS_DEVICE);
+    dn_vae* h = new dn_vae();
+    h->v = v;
+    *out = h;
+  });
+}
+
+dn_status dn_vae_decode(dn_vae* h, const float* latent, float* image, void* stream) {
+  return guarded([&] {
+    DN_CHECK(h && h->v, "dn_vae_decode: null handle");
+    dn::vae_decode(h->v, latent, image, as_stream(stream));
+  });
+}
+
+void dn_vae_destroy(dn_vae* h) {
+  if (!h) return;
+  dn::vae_destroy(h->v);
+  delete h;
 }
 
 void dn_destroy(dn_handle* h) {

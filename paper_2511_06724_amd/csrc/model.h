@@ -37,4 +37,11 @@ void model_denoise(Model* m, float* latent, const float* ctx, const int32_t* ts,
 void model_unet_eps(Model* m, const float* x, int t, const float* ctx, float scale, float* raw, float* guided,
                     hipStream_t s);
 
+// Latent decoder (vae.hip).
+struct Vae;
+std::vector<TensorSpec> vae_weight_table(const dn_vae_config& cfg);
+Vae* vae_create(const dn_vae_config& cfg, const float* weights, size_t n_floats, bool on_device);
+void vae_decode(Vae* v, const float* latent, float* image, hipStream_t s);
+void vae_destroy(Vae* v);
+
 }  // namespace dn

@@ -11,7 +11,7 @@ import os
 
 import numpy as np
 
-from .workloads import DnConfig
+from .workloads import DnConfig, VaeConfig
 
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libargus_dn.so")
 
@@ -24,7 +24,8 @@ MAX_LEVELS = 4
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_denoise_capture", "dn_unet_eps", "ac_lookup",
             "ac_lookup_batch", "ac_lookup_batch_k", "ac_lookup_batch_noalloc", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
             "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_layernorm_slabs", "dn_op_linear_vt",
-            "dn_destroy", "dn_last_error", "argus_oda", "argus_route", "argus_select_worker", "argus_last_error")
+            "dn_destroy", "dn_last_error", "dn_vae_weight_count", "dn_vae_weight_table", "dn_vae_create",
+            "dn_vae_decode", "dn_vae_destroy", "argus_oda", "argus_route", "argus_select_worker", "argus_last_error")
 
 
 AC_MAX_K_LEVELS = 16
@@ -55,6 +56,15 @@ class _Config(C.Structure):
         ("gn_eps", C.c_float), ("tx_gn_eps", C.c_float), ("ln_eps", C.c_float),
         ("n_train_steps", C.c_int32), ("beta_start", C.c_float), ("beta_end", C.c_float),
         ("beta_schedule", C.c_int32),
+    ]
+
+
+class _VaeConfig(C.Structure):
+    _fields_ = [
+        ("abi_version", C.c_int32), ("dtype", C.c_int32), ("batch", C.c_int32),
+        ("latent_c", C.c_int32), ("latent_h", C.c_int32), ("latent_w", C.c_int32),
+        ("n_levels", C.c_int32), ("channels", C.c_int32 * MAX_LEVELS), ("layers_per_block", C.c_int32),
+        ("gn_groups", C.c_int32), ("gn_eps", C.c_float), ("scaling_factor", C.c_float), ("out_c", C.c_int32),
     ]
 
 
@@ -93,6 +103,11 @@ def _load():
         "argus_route": [P, I32, I32, C.c_double, C.POINTER(I32)],
         "argus_select_worker": [P, P, P, I32, I32, C.POINTER(I32)],
         "argus_last_error": [],
+        "dn_vae_weight_count": [C.POINTER(_VaeConfig), C.POINTER(SZ)],
+        "dn_vae_weight_table": [C.POINTER(_VaeConfig), P, P, P, SZ, C.POINTER(SZ)],
+        "dn_vae_create": [C.POINTER(_VaeConfig), P, SZ, I32, C.POINTER(P)],
+        "dn_vae_decode": [P, P, P, P],
+        "dn_vae_destroy": [P],
         "dn_destroy": [P],
         "dn_last_error": [],
     }
@@ -101,6 +116,7 @@ def _load():
         f.argtypes = args
         f.restype = C.c_int
     lib.dn_destroy.restype = None
+    lib.dn_vae_destroy.restype = None
     lib.dn_last_error.restype = C.c_char_p
     lib.argus_last_error.restype = C.c_char_p
     return lib
@@ -214,6 +230,62 @@ class Denoiser:
     def unet_eps(self, x, t, text_ctx, cfg_scale, out_raw, out_guided=None, stream=None):
         _check(lib.dn_unet_eps(self._h, _ptr(x), int(t), _ptr(text_ctx), cfg_scale, _ptr(out_raw),
                                _ptr(out_guided), _stream(stream)))
+
+
+def to_c_vae_config(cfg: VaeConfig) -> _VaeConfig:
+    c = _VaeConfig()
+    c.abi_version = ABI_VERSION
+    c.dtype, c.batch = cfg.dtype, cfg.batch
+    c.latent_c, c.latent_h, c.latent_w = cfg.latent_c, cfg.latent_h, cfg.latent_w
+    c.n_levels = len(cfg.block_channels)
+    for i, ch in enumerate(cfg.block_channels):
+        c.channels[i] = ch
+    c.layers_per_block, c.gn_groups, c.gn_eps = cfg.layers_per_block, cfg.gn_groups, cfg.gn_eps
+    c.scaling_factor, c.out_c = cfg.scaling_factor, cfg.out_c
+    return c
+
+
+def vae_weight_table(cfg):
+    """[(numel, fan_in, kind)] of the decoder's canonical blob."""
+    c = to_c_vae_config(cfg)
+    n = C.c_size_t()
+    _check(lib.dn_vae_weight_table(C.byref(c), None, None, None, 0, C.byref(n)))
+    numel = np.zeros(n.value, np.int64)
+    fan = np.zeros(n.value, np.int32)
+    kind = np.zeros(n.value, np.int32)
+    _check(lib.dn_vae_weight_table(C.byref(c), numel.ctypes.data, fan.ctypes.data, kind.ctypes.data, n.value,
+                                   C.byref(n)))
+    return list(zip(numel.tolist(), fan.tolist(), kind.tolist()))
+
+
+class Decoder:
+    """Owns a dn_vae. ``weights``: fp32 numpy array (host) or CUDA tensor (device)."""
+
+    def __init__(self, cfg: VaeConfig, weights):
+        self.cfg = cfg
+        self._h = C.c_void_p()
+        on_dev = not isinstance(weights, np.ndarray)
+        if on_dev:
+            n = weights.numel()
+        else:
+            weights = np.ascontiguousarray(weights, dtype=np.float32)
+            n = weights.size
+        _check(lib.dn_vae_create(C.byref(to_c_vae_config(cfg)), _ptr(weights), n,
+                                 DN_WEIGHTS_DEVICE if on_dev else DN_WEIGHTS_HOST, C.byref(self._h)))
+
+    def decode(self, latent, image, stream=None):
+        _check(lib.dn_vae_decode(self._h, _ptr(latent), _ptr(image), _stream(stream)))
+
+    def close(self):
+        if self._h:
+            lib.dn_vae_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def ac_lookup(query, cache):

@@ -76,6 +76,39 @@ def sdxl_small(dtype=DN_BF16, batch=1):
                     levels=((320, 0, 5, 64), (640, 1, 10, 64), (1280, 4, 20, 64)), mid_depth=4)
 
 
+@dataclass
+class VaeConfig:
+    """Mirror of the C ``dn_vae_config`` struct: the latent decoder run once per image
+    after the denoise loop (Table 3's VAE Decoder)."""
+    dtype: int = DN_BF16
+    batch: int = 1
+    latent_c: int = 4
+    latent_h: int = 128
+    latent_w: int = 128
+    block_channels: tuple = (128, 256, 512, 512)   # level widths, slowest-resolution last
+    layers_per_block: int = 2                       # the up path runs layers_per_block + 1 ResBlocks per level
+    gn_groups: int = 32
+    gn_eps: float = 1e-6
+    scaling_factor: float = 0.13025                 # the latent is divided by it before decoding
+    out_c: int = 3
+
+    def with_(self, **kw):
+        return replace(self, **kw)
+
+
+def sd_vae(dtype=DN_BF16, latent=128, batch=1):
+    """The SD / SD-XL latent decoder: widths 128, 256, 512, 512, three ResBlocks per up
+    level, one-head attention in the middle block; latent x latent -> 8x larger RGB image
+    (128 -> 1024 x 1024 for SD-XL; 64 -> 512 x 512, the size Table 3 counts)."""
+    return VaeConfig(dtype=dtype, batch=batch, latent_h=latent, latent_w=latent)
+
+
+def tiny_vae(dtype=DN_FP32):
+    """A two-level decoder (widths 64, 128, one ResBlock pair per level): 8x8 latent ->
+    16x16 image. Same module types as the full decoder, small enough for exact checks."""
+    return VaeConfig(dtype=dtype, batch=1, latent_h=8, latent_w=8, block_channels=(64, 128), layers_per_block=1)
+
+
 def sd20_shape():
     """SD 2.0 UNet topology (4 levels, linear projections, context 1024). Used only
     for the parameter / FLOP pins of Table 3; not a benchmark workload."""
