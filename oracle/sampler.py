@@ -20,16 +20,17 @@ def abar_table(cfg):
     return S.alphas_cumprod(S.betas(cfg.n_train_steps, cfg.beta_start, cfg.beta_end, cfg.beta_schedule))
 
 
-def step(cfg, W, x, ctx, t, t_prev, cfg_scale, abar=None):
+def step(cfg, W, x, ctx, t, t_prev, cfg_scale, abar=None, ff_act=None):
     """One guided DDIM iteration for a batch of B latents.
 
     x [B, c, H, W] fp32; ctx [2B, L, D] = B unconditional then B conditional rows.
     The UNet runs once on [x; x] (effective batch 2B). Returns
-    (eps_raw [2B, c, H, W], eps_guided [B, c, H, W], x_next [B, c, H, W])."""
+    (eps_raw [2B, c, H, W], eps_guided [B, c, H, W], x_next [B, c, H, W]). ff_act: the
+    quantized variant's rounding of the feed-forward inputs (unet.transformer)."""
     if abar is None:
         abar = abar_table(cfg)
     b = x.shape[0]
-    eps_raw = forward(cfg, W, np.concatenate([x, x], axis=0), t, ctx)
+    eps_raw = forward(cfg, W, np.concatenate([x, x], axis=0), t, ctx, ff_act)
     eps = S.cfg(eps_raw[:b], eps_raw[b:], cfg_scale)
     x_next = S.ddim_step(x, eps, S.abar_at(abar, t), S.abar_at(abar, t_prev))
     return eps_raw, eps, x_next.astype(np.float32)

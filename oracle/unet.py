@@ -73,7 +73,9 @@ def resblock(cfg, W, p, x, temb):
     return x + h
 
 
-def transformer(cfg, W, p, x, ctx, depth, heads):
+def transformer(cfg, W, p, x, ctx, depth, heads, ff_act=None):
+    """ff_act: None, or the rounding the quantized variant applies to the feed-forward's
+    two inputs (the third LayerNorm's output and the GEGLU output)."""
     n, c, hh, ww = x.shape
     h = L.group_norm(x, cfg.gn_groups, W[p + ".gn.g"], W[p + ".gn.b"], cfg.tx_gn_eps)
     h = h.reshape(n, c, hh * ww).transpose(0, 2, 1)          # tokens in row-major (y, x) order
@@ -87,14 +89,21 @@ def transformer(cfg, W, p, x, ctx, depth, heads):
         h = h + L.attention(a, ctx, W[b + ".attn2.q.w"], W[b + ".attn2.k.w"], W[b + ".attn2.v.w"],
                             W[b + ".attn2.o.w"], W[b + ".attn2.o.b"], heads)
         a = L.layer_norm(h, W[b + ".ln3.g"], W[b + ".ln3.b"], cfg.ln_eps)
-        h = h + L.geglu_ff(a, W[b + ".ff1.w"], W[b + ".ff1.b"], W[b + ".ff2.w"], W[b + ".ff2.b"])
+        if ff_act is None:
+            h = h + L.geglu_ff(a, W[b + ".ff1.w"], W[b + ".ff1.b"], W[b + ".ff2.w"], W[b + ".ff2.b"])
+        else:
+            u = L.linear(ff_act(a), W[b + ".ff1.w"], W[b + ".ff1.b"])
+            half = u.shape[-1] // 2
+            g = ff_act(u[..., :half] * L.gelu(u[..., half:]))
+            h = h + L.linear(g, W[b + ".ff2.w"], W[b + ".ff2.b"])
     h = L.linear(h, W[p + ".proj_out.w"], W[p + ".proj_out.b"])
     return x + h.transpose(0, 2, 1).reshape(n, c, hh, ww)
 
 
-def forward(cfg, W, x, t, ctx):
+def forward(cfg, W, x, t, ctx, ff_act=None):
     """eps_theta for a batch: x [n, latent_c, H, W] fp32, scalar timestep t,
-    ctx [n, ctx_len, ctx_dim] fp32 -> [n, latent_c, H, W] fp32. W from ``unpack``."""
+    ctx [n, ctx_len, ctx_dim] fp32 -> [n, latent_c, H, W] fp32. W from ``unpack``;
+    ff_act as in ``transformer``."""
     x = np.asarray(x, dtype=np.float32)
     ctx = np.asarray(ctx, dtype=np.float32)
     temb = None
@@ -114,7 +123,7 @@ def forward(cfg, W, x, t, ctx):
             h = resblock(cfg, W, op[1], h, temb)
         elif kind == "tx":
             _, p, _, depth, heads = op
-            h = transformer(cfg, W, p, h, ctx, depth, heads)
+            h = transformer(cfg, W, p, h, ctx, depth, heads, ff_act)
         elif kind == "down":
             h = L.conv2d(h, W[op[1] + ".w"], W[op[1] + ".b"], stride=2)
         elif kind == "up":
