@@ -63,7 +63,7 @@ typedef enum {
   DN_EUNSUPPORTED = -4  /* valid but not supported by this build (e.g. no gfx950 device) */
 } dn_status;
 
-typedef enum { DN_FP32 = 0, DN_BF16 = 1 } dn_dtype;
+typedef enum { DN_FP32 = 0, DN_BF16 = 1, DN_FP8 = 2 } dn_dtype;
 typedef enum { DN_WEIGHTS_HOST = 0, DN_WEIGHTS_DEVICE = 1 } dn_weights_location;
 typedef enum { DN_BETA_LINEAR = 0, DN_BETA_SCALED_LINEAR = 1 } dn_beta_schedule;
 
@@ -84,6 +84,12 @@ typedef struct {
  *                norm statistics, softmax, the time embedding, the transformer
  *                residual stream, the latent and the DDIM update stay fp32.
  *                DN_FP32: everything fp32.
+ *                DN_FP8: the quantized variant (quantized models are approximation
+ *                levels, Sec. 4.2): DN_BF16 except the GEGLU feed-forward of every
+ *                transformer block, whose two matrices are OCP E4M3 codes with one
+ *                fp32 scale per output row (row max / 448) and whose two inputs (the
+ *                third LayerNorm's output, the GEGLU output) are E4M3 at scale 1
+ *                (nearest even, saturating at 448), multiplied on the fp8 matrix cores.
  * batch          images B; the UNet runs on 2B rows (B unconditional, then B
  *                conditional) for classifier-free guidance.
  * latent_*       latent channels (<= 64) and spatial size; H and W must be
@@ -307,7 +313,12 @@ dn_status ac_fetch_latent(const uint16_t* cache_latents, int64_t n, int64_t nume
  *   up to 32, times K, for the fragment order; N * K otherwise).
  * dn_pack_weight: packs a row-major device matrix w [N][K] (dtype elements) into
  *   `out` (device, dn_packed_weight_elems elements, not overlapping w). K must be a
- *   multiple of 16. Asynchronous on `stream`. */
+ *   multiple of 16. Asynchronous on `stream`.
+ * DN_FP8: w is fp32 [N][K] (N % 32 == 0, K % 128 == 0); `out` receives N * K bytes of
+ *   E4M3 codes in the fragment order of the 32x32x64 fp8 matrix-core step (per 32 rows
+ *   and 64-deep step, the lanes' 32-byte operands in 2 KB), code = round(w / scale_n),
+ *   then N fp32 scales scale_n = max_k |w[n][k]| / 448 (1 for a zero row);
+ *   dn_packed_weight_elems gives the total in bytes. */
 dn_status dn_packed_weight_elems(int32_t dtype, int32_t N, int32_t K, int64_t* elems);
 dn_status dn_pack_weight(int32_t dtype, const void* w, int32_t N, int32_t K, void* out, void* stream);
 
@@ -321,7 +332,11 @@ dn_status dn_pack_weight(int32_t dtype, const void* w, int32_t N, int32_t K, voi
  * entries, interleaved in blocks of 32 — rows [64j, 64j+32) are value rows
  * [32j, 32j+32) and rows [64j+32, 64j+64) the matching gate rows — and
  * y[m][n] = a * GELU(g) with a, g the value and gate outputs of column n
- * (exact erf GELU); N % 32 == 0 and resid must be NULL. Asynchronous. */
+ * (exact erf GELU); N % 32 == 0 and resid must be NULL. Asynchronous.
+ * DN_FP8: x E4M3 codes [M][K], w packed for DN_FP8 (K % 128 == 0; GEGLU value / gate
+ *   rows interleaved as above before packing), accumulator column n scaled by scale_n;
+ *   y fp32 when y_f32 != 0, else E4M3 codes when geglu != 0 (the input of the next fp8
+ *   layer), else bf16; resid fp32 or bf16 per resid_f32. */
 dn_status dn_op_linear(int32_t dtype, const void* x, const void* w, const float* bias, const void* resid,
                        int32_t resid_f32, void* y, int32_t y_f32, int64_t M, int32_t N, int32_t K, int32_t geglu,
                        void* stream);
@@ -373,7 +388,8 @@ dn_status dn_op_groupnorm(int32_t dtype, const void* x, void* y, int32_t n, int3
                           const float* gamma, const float* beta, float eps, int32_t silu, void* stream);
 
 /* LayerNorm over the last axis: x fp32 [M][C] (the residual stream), y [M][C]
- * in `dtype`; C a multiple of 4, at most 2048. Asynchronous. */
+ * in `dtype` (E4M3 codes for DN_FP8, nearest even, saturating); C a multiple of 4, at
+ * most 2048. Asynchronous. */
 dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int32_t C, const float* gamma,
                           const float* beta, float eps, void* stream);
 

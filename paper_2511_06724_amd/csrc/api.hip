@@ -183,6 +183,7 @@ void lookup_batch_host(const uint16_t* query_embs, int32_t nq, const uint16_t* c
 }
 
 bool is_dtype(int32_t d) { return d == DN_FP32 || d == DN_BF16; }
+bool is_dtype8(int32_t d) { return is_dtype(d) || d == DN_FP8; }
 
 // Per-device state of the single-kernel GEMM entry points: CU count (tile
 // planning) and a zero block for implicit-conv padding reads.
@@ -224,6 +225,11 @@ OpDev& op_dev_locked(int dev) {
   return d;
 }
 
+template <typename T> dn::GemmPlan op_plan(const dn::GemmParams& p, int cus) {
+  return p.wscale ? dn::gemm_plan_fp8(p.M, p.N, p.K, p.geglu, cus, true, false)
+                  : dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, cus, p.vt == nullptr, false, p.taps == 9);
+}
+
 template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
   int dev = 0;
   DN_HIP(hipGetDevice(&dev));
@@ -231,15 +237,18 @@ template <typename T> void op_gemm(dn::GemmParams& p, hipStream_t s) {
   {
     std::lock_guard<std::mutex> lk(g_op_mu);
     OpDev& d = op_dev_locked(dev);
-    const dn::GemmPlan g0 = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, d.cus, p.vt == nullptr, false, p.taps == 9);
+    const dn::GemmPlan g0 = op_plan<T>(p, d.cus);
     grow(&d.part, &d.part_floats, dn::gemm_workspace_floats(g0, p.M, p.N));
     w = d;
   }
-  const dn::GemmPlan g = dn::gemm_plan<T>(p.M, p.N, p.K, p.geglu, w.cus, p.vt == nullptr, false, p.taps == 9);
+  const dn::GemmPlan g = op_plan<T>(p, w.cus);
   p.zero16 = w.zero;
   p.part = w.part;
   p.part_floats = w.part_floats;
-  dn::gemm<T>(p, g, s);
+  if (p.wscale)
+    dn::gemm_fp8(p, g, s);
+  else
+    dn::gemm<T>(p, g, s);
 }
 
 }  // namespace
@@ -403,17 +412,36 @@ dn_status ac_fetch_latent(const uint16_t* cache_latents, int64_t n, int64_t nume
 
 dn_status dn_packed_weight_elems(int32_t dtype, int32_t N, int32_t K, int64_t* elems) {
   return guarded([&] {
-    DN_CHECK(is_dtype(dtype), "dn_packed_weight_elems: bad dtype");
+    DN_CHECK(is_dtype8(dtype), "dn_packed_weight_elems: bad dtype");
     DN_CHECK(elems, "dn_packed_weight_elems: null pointer");
     DN_CHECK(N >= 1 && K >= 1, "dn_packed_weight_elems: bad sizes");
+    if (dtype == DN_FP8) {
+      DN_CHECK(dn::gemm_fp8_layout(N, K), "dn_packed_weight_elems: DN_FP8 needs N % 32 == 0, K % 128 == 0");
+      *elems = (int64_t)dn::gemm_fp8_code_bytes(N, K) + 4ll * N;
+      return;
+    }
     *elems = dtype == DN_BF16 && dn::gemm_frag_layout(N, K) ? (int64_t)dn::gemm_frag_elems(N, K) : (int64_t)N * K;
   });
 }
 
 dn_status dn_pack_weight(int32_t dtype, const void* w, int32_t N, int32_t K, void* out, void* stream) {
   return guarded([&] {
-    DN_CHECK(is_dtype(dtype), "dn_pack_weight: bad dtype");
+    DN_CHECK(is_dtype8(dtype), "dn_pack_weight: bad dtype");
     DN_CHECK(w && out, "dn_pack_weight: null pointer");
+    if (dtype == DN_FP8) {
+      DN_CHECK(dn::gemm_fp8_layout(N, K), "dn_pack_weight: DN_FP8 needs N % 32 == 0, K % 128 == 0");
+      dn::PackParams p;
+      p.dst = out;
+      p.rows = N;
+      p.cols = K;
+      p.ld_dst = K;
+      p.src = static_cast<const float*>(w);
+      p.src_rows = N;
+      p.src_cols = K;
+      dn::pack_fp8(p, reinterpret_cast<float*>(static_cast<char*>(out) + dn::gemm_fp8_code_bytes(N, K)),
+                   as_stream(stream));
+      return;
+    }
     DN_CHECK(N >= 1 && K >= 1 && K % 16 == 0, "dn_pack_weight: bad sizes (K must be a multiple of 16)");
     if (dtype == DN_BF16 && dn::gemm_frag_layout(N, K)) {
       dn::to_frag(static_cast<const dn::bf16*>(w), N, K, K, static_cast<dn::bf16*>(out), as_stream(stream));
@@ -428,7 +456,7 @@ dn_status dn_op_linear(int32_t dtype, const void* x, const void* w, const float*
                        int32_t resid_f32, void* y, int32_t y_f32, int64_t M, int32_t N, int32_t K, int32_t geglu,
                        void* stream) {
   return guarded([&] {
-    DN_CHECK(is_dtype(dtype), "dn_op_linear: bad dtype");
+    DN_CHECK(is_dtype8(dtype), "dn_op_linear: bad dtype");
     DN_CHECK(x && w && y, "dn_op_linear: null pointer");
     DN_CHECK(M >= 1 && M <= 0x7fffffff && N >= 1 && K >= 1, "dn_op_linear: bad sizes");
     DN_CHECK(!geglu || N % 32 == 0, "dn_op_linear: GEGLU needs N % 32 == 0");
@@ -452,10 +480,17 @@ dn_status dn_op_linear(int32_t dtype, const void* x, const void* w, const float*
     p.out_f32 = y_f32;
     p.n_store = N;
     p.geglu = geglu;
-    if (dtype == DN_BF16)
+    if (dtype == DN_FP8) {
+      const int Nw = geglu ? 2 * N : N;
+      DN_CHECK(dn::gemm_fp8_layout(Nw, K), "dn_op_linear: DN_FP8 needs N % 32 == 0 and K % 128 == 0");
+      p.wscale = reinterpret_cast<const float*>(static_cast<const char*>(w) + dn::gemm_fp8_code_bytes(Nw, K));
+      p.out_fp8 = !y_f32 && geglu;
       op_gemm<dn::bf16>(p, as_stream(stream));
-    else
+    } else if (dtype == DN_BF16) {
+      op_gemm<dn::bf16>(p, as_stream(stream));
+    } else {
       op_gemm<float>(p, as_stream(stream));
+    }
   });
 }
 
@@ -615,9 +650,11 @@ dn_status dn_op_groupnorm(int32_t dtype, const void* x, void* y, int32_t n, int3
 dn_status dn_op_layernorm(int32_t dtype, const float* x, void* y, int64_t M, int32_t C, const float* gamma,
                           const float* beta, float eps, void* stream) {
   return guarded([&] {
-    DN_CHECK(is_dtype(dtype), "dn_op_layernorm: bad dtype");
+    DN_CHECK(is_dtype8(dtype), "dn_op_layernorm: bad dtype");
     DN_CHECK(x && y && gamma && beta, "dn_op_layernorm: null pointer");
-    if (dtype == DN_BF16)
+    if (dtype == DN_FP8)
+      dn::layernorm<uint8_t>(x, static_cast<uint8_t*>(y), M, C, gamma, beta, eps, as_stream(stream));
+    else if (dtype == DN_BF16)
       dn::layernorm<dn::bf16>(x, static_cast<dn::bf16*>(y), M, C, gamma, beta, eps, as_stream(stream));
     else
       dn::layernorm<float>(x, static_cast<float*>(y), M, C, gamma, beta, eps, as_stream(stream));

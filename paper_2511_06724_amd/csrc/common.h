@@ -65,6 +65,16 @@ __device__ __forceinline__ float gelu_erf(float x) {
   return 0.5f * x * (1.0f + copysignf(e, x));
 }
 
+// Four floats -> four OCP E4M3 codes (nearest even) in one 32-bit word, byte e = value e.
+// The hardware conversion turns magnitudes beyond the format into NaN codes, so values
+// are clamped to +-448 first: the conversion then saturates.
+__device__ __forceinline__ unsigned fp8x4(float a, float b, float c, float d) {
+  const float lo = -448.f, hi = 448.f;
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(fminf(fmaxf(a, lo), hi), fminf(fmaxf(b, lo), hi), 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(fminf(fmaxf(c, lo), hi), fminf(fmaxf(d, lo), hi), w, true);
+  return static_cast<unsigned>(w);
+}
+
 // 16-byte vector load/store helpers.
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }

@@ -293,9 +293,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
 
   // Epilogue input of the plain path (the residual or the per-sample row vector, when
   // exactly one is present) for small wave tiles of the linear modes without stage
-  // read-ahead (where the registers are free): loaded before the main loop, whose
-  // latency then hides the load, into FM x ENP x 2 16-byte registers per lane, in the
-  // layout of the row-contiguous epilogue (8 consecutive columns per lane).
+  // read-ahead (where the registers are free): loaded into FM x ENP x 2 16-byte registers
+  // per lane, in the layout of the row-contiguous epilogue (8 consecutive columns per
+  // lane). The loads are issued right after the prologue's A and B loads, so the first
+  // wait (in-order vector-memory counter) does not include them and the main loop's
+  // latency hides them.
   constexpr int ELPR = WN / 8;     // lanes per row in the row-contiguous epilogue
   constexpr int ERPI = 64 / ELPR;  // rows per pass
   constexpr int ENP = 32 / ERPI;   // passes per 32-row block
@@ -304,27 +306,29 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   const bool pre_in = kPreIn && !p.geglu && !(p.vt && enw0 + WN > p.vt_col0) &&
                       ((p.resid != nullptr) != (p.rowvec != nullptr));
   f32x4 pin[kPreIn ? FM : 1][kPreIn ? ENP : 1][2];
-  if constexpr (kPreIn) {
-    if (pre_in) {
-      const int n = enw0 + (lane % ELPR) * 8;
-      const bool rvec = n + 8 <= p.n_store && p.resid && resid_vec8(p);
+  auto load_pre_in = [&]() {
+    if constexpr (kPreIn) {
+      if (pre_in) {
+        const int n = enw0 + (lane % ELPR) * 8;
+        const bool rvec = n + 8 <= p.n_store && p.resid && resid_vec8(p);
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+        for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int t = 0; t < ENP; ++t) {
-          const int m = m0 + i * 32 + t * ERPI + lane / ELPR;
-          float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-          if (m < p.M && n < p.n_store) {
-            if (p.rowvec)
-              load_rowvec8(p, m, n, v);
-            else
-              load_resid8(p, m, n, rvec, v);
+          for (int t = 0; t < ENP; ++t) {
+            const int m = m0 + i * 32 + t * ERPI + lane / ELPR;
+            float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            if (m < p.M && n < p.n_store) {
+              if (p.rowvec)
+                load_rowvec8(p, m, n, v);
+              else
+                load_resid8(p, m, n, rvec, v);
+            }
+            pin[i][t][0] = f32x4{v[0], v[1], v[2], v[3]};
+            pin[i][t][1] = f32x4{v[4], v[5], v[6], v[7]};
           }
-          pin[i][t][0] = f32x4{v[0], v[1], v[2], v[3]};
-          pin[i][t][1] = f32x4{v[4], v[5], v[6], v[7]};
-        }
+      }
     }
-  }
+  };
 
   // A fragment of k-step s: row (lane % 32) of each 32-row block, logical chunk
   // 2 s + (lane / 32) at its swizzled position.
@@ -423,6 +427,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
     for (int d = 0; d < D; ++d)
   #pragma unroll
       for (int s = 0; s < 4; ++s) load_b_step(kt0 + d, s, bq[d]);
+    // the epilogue inputs come after every prologue load: the waits below count only
+    // loads issued after their target, so more of them (these) keep the waits exact or
+    // conservative
+    load_pre_in();
     __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((S - 1 - Q) * PW + D * 4 * FN));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
@@ -713,6 +721,330 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   throw Error(-1, "gemm: no fragment-B kernel for this tile plan");
 }
 
+// ---------------------------------------------------------------- fp8 (E4M3) kernel
+//
+// The same organisation as gemm_frag_kernel for E4M3 operands on the 32x32x64 fp8
+// matrix-core step (v_mfma_scale_f32_32x32x64_f8f6f4 with unit block scales): an LDS
+// stage still holds 128-byte rows, now 128 k-values, i.e. two matrix-core steps; lane l
+// supplies row (l % 32) and the 32 consecutive k-values 32 (l / 32) .. + 32 of a step
+// (two 16-byte LDS reads; any k order common to both operands gives the same sum).
+// B is packed by pack_fp8: per 32 output rows and 64-deep step, the lanes' 32-byte
+// operands in 2 KB. The epilogue multiplies each column by its row scale of B.
+typedef int v8i __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ v8i v8i_of(const uint4& a, const uint4& b) {
+  v8i r;
+  r[0] = (int)a.x, r[1] = (int)a.y, r[2] = (int)a.z, r[3] = (int)a.w;
+  r[4] = (int)b.x, r[5] = (int)b.y, r[6] = (int)b.z, r[7] = (int)b.w;
+  return r;
+}
+
+// Eight outputs [n, n + 8) of row m as E4M3 codes (8 bytes), or element-wise past n_store.
+__device__ __forceinline__ void store8_fp8(const GemmParams& p, int m, int n, const float v[8]) {
+  uint8_t* o = static_cast<uint8_t*>(p.out) + (long long)m * p.ldo + n;
+  if (n + 8 <= p.n_store && ((reinterpret_cast<__UINTPTR_TYPE__>(o) & 7) == 0)) {
+    uint2 w;
+    w.x = fp8x4(v[0], v[1], v[2], v[3]);
+    w.y = fp8x4(v[4], v[5], v[6], v[7]);
+    *reinterpret_cast<uint2*>(o) = w;
+  } else {
+    for (int e = 0; e < 8; ++e)
+      if (n + e < p.n_store) o[e] = static_cast<uint8_t>(fp8x4(v[e], 0.f, 0.f, 0.f) & 0xff);
+  }
+}
+
+template <int BM, int FN, int S, int WPE, bool SPLIT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_fp8_kernel(
+    GemmParams p, int mt, int nt, int nsplit) {
+  constexpr int NW = 4;
+  constexpr int FM = BM / 32;
+  constexpr int WN = 32 * FN;
+  constexpr int BN = NW * WN;
+  constexpr int STAGE = BM * kRowBytes;
+  constexpr int PW = BM / 32;  // DMA instructions (8 rows of 128 B) per wave per stage
+  constexpr int NM = FM * FN;
+  static_assert(S >= 3 && S <= 4, "three or four LDS stages");
+
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int units = mt * nt * nsplit;
+  const int wg = blockIdx.x;
+  const int xcd = wg % kXcds, idx = wg / kXcds;
+  const int base = units / kXcds, rem = units % kXcds;
+  const int logical = xcd * base + min(xcd, rem) + idx;
+  const int m_tile = logical % mt;
+  const int ns = logical / mt;
+  const int split = ns % nsplit;
+  const int n_tile = ns / nsplit;
+  const int n0 = n_tile * BN, m0 = m_tile * BM;
+  const int nk = p.K / 128;
+  const int kt0 = (int)((long long)split * nk / nsplit);
+  const int kt1 = (int)((long long)(split + 1) * nk / nsplit);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+  // A rows: DMA instruction j of this wave fills tile rows [8 q, 8 q + 8), q = wave PW + j
+  const int lrow = lane >> 3;
+  const int lc_even = ((lane & 7) ^ lrow) * 16, lc_odd = ((lane & 7) ^ lrow ^ 1) * 16;
+  int off0[PW];
+#pragma unroll
+  for (int j = 0; j < PW; ++j) {
+    const int q = wave * PW + j;
+    const int m = min(m0 + 8 * q + lrow, p.M - 1);
+    off0[j] = m * p.lda0 + ((q & 1) ? lc_odd : lc_even);
+  }
+  const uint8_t* const gA = static_cast<const uint8_t*>(p.a0);
+  auto issue_a = [&](int kt_in, int slot) {
+    const bool real = kt_in < kt1;
+    unsigned char* stage = smem + slot * STAGE;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int q = wave * PW + j;
+      const uint8_t* g = real ? gA + off0[j] + kt_in * 128 : static_cast<const uint8_t*>(p.zero16);
+      dma16(g, (lds_void*)(stage + q * 1024));
+    }
+  };
+
+  // B operands of this wave: column blocks nb = (n0 + wave WN) / 32 + j (clamped)
+  const int ksteps = p.K / 64;
+  const int nb_last = (p.N + 31) / 32 - 1;
+  const uint8_t* bptr[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int nb = min((n0 + wave * WN) / 32 + j, nb_last);
+    bptr[j] = static_cast<const uint8_t*>(p.b) + (long long)nb * ksteps * 2048 + lane * 32;
+  }
+  typedef uint4 BStep[FN][2];  // one 64-deep step: FN column blocks, 32 bytes per lane
+  auto load_b = [&](int step_in, BStep& dst) {
+    const int st = step_in < 2 * kt1 ? step_in : 2 * kt1 - 1;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const uint8_t* src = bptr[j] + (long long)st * 2048;
+      dst[j][0] = *reinterpret_cast<const uint4*>(src);
+      dst[j][1] = *reinterpret_cast<const uint4*>(src + 16);
+    }
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int frow = lane & 31;
+  const int fs = (lane & 7) ^ ((lane >> 3) & 1);
+  const int hh = lane >> 5;
+  auto read_a = [&](int slot, int s2, v8i* a) {
+    const unsigned char* st = smem + slot * STAGE + frow * kRowBytes;
+    const int c0 = 4 * s2 + 2 * hh;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const uint4 lo = *reinterpret_cast<const uint4*>(st + i * 32 * kRowBytes + ((c0 ^ fs) * 16));
+      const uint4 hi = *reinterpret_cast<const uint4*>(st + i * 32 * kRowBytes + (((c0 + 1) ^ fs) * 16));
+      a[i] = v8i_of(lo, hi);
+    }
+  };
+  auto mfmas = [&](const v8i* a, const BStep& b) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(v8i_of(b[j][0], b[j][1]), a[i], acc[i][j], 0, 0,
+                                                                    0, 127, 0, 127);
+  };
+
+  // Prologue: A stages kt0 .. kt0 + 1, then B of step 2 kt0. Stage kt (r = kt - kt0):
+  // wait until this wave's DMA of stage kt landed, barrier, DMA of stage kt + 2 into the
+  // slot of stage kt - 1, B of step 2 kt + 1, step 2 kt, B of step 2 kt + 2, step 2 kt + 1
+  // (B is loaded one 64-deep step ahead). Loads issued after the DMA of stage kt: from
+  // the prologue PW + 2 FN (r = 0) and PW + 6 FN (r = 1); in steady state (r >= 2) the
+  // 4 FN B loads of the stage that issued it and one whole stage, PW + 8 FN.
+  static_assert(S == 3, "three LDS stages");
+  constexpr int W0 = PW + 2 * FN;
+  constexpr int W1 = PW + 6 * FN;
+  constexpr int WS = PW + 8 * FN;
+  static_assert(WS < 64, "vmcnt range");
+  issue_a(kt0, 0);
+  issue_a(kt0 + 1, 1);
+  BStep b0, b1;
+  load_b(2 * kt0, b0);
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int r = kt - kt0;
+    if (r == 0)
+      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(W0));
+    else if (r == 1)
+      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(W1));
+    else
+      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(WS));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue_a(kt + 2, (r + 2) % 3);
+    const int slot = r % 3;
+    v8i a[FM];
+    load_b(2 * kt + 1, b1);
+    read_a(slot, 0, a);
+    mfmas(a, b0);
+    KSched<0, NM, 0, 0>::apply();
+    __builtin_amdgcn_sched_barrier(0);
+    load_b(2 * kt + 2, b0);
+    read_a(slot, 1, a);
+    mfmas(a, b1);
+    KSched<0, NM, 0, 0>::apply();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+  __syncthreads();
+
+  // ---- epilogue (row-contiguous through LDS, as gemm_frag_kernel), columns scaled
+  const int col = lane & 31;
+  const int h4 = 4 * (lane >> 5);
+  const int nw0 = n0 + wave * WN;
+  constexpr int EPL = WN + 4;
+  float* ep = reinterpret_cast<float*>(smem) + wave * (32 * EPL);
+  float* slab = SPLIT ? p.part + (long long)split * p.M * p.n_store : nullptr;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(ep + col * EPL + j * 32 + 8 * g + h4) =
+            f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+    const int mb = m0 + i * 32;
+    if (SPLIT) {
+      constexpr int LPR = WN / 4;
+      constexpr int RPI = 64 / LPR;
+      const int c4 = (lane % LPR) * 4;
+      const int n = nw0 + c4;
+      float sc[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sc[e] = n + e < p.n_store ? p.wscale[n + e] : 0.f;
+#pragma unroll
+      for (int t = 0; t < 32 / RPI; ++t) {
+        const int rr = t * RPI + lane / LPR;
+        f32x4 v4 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c4);
+        const int m = mb + rr;
+        if (m >= p.M || n >= p.n_store) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] *= sc[e];
+        *reinterpret_cast<f32x4*>(slab + (long long)m * p.n_store + n) = v4;
+      }
+    } else if (!p.geglu) {
+      constexpr int LPR = WN / 8;
+      constexpr int RPI = 64 / LPR;
+      constexpr int NP = 32 / RPI;
+      const int c8 = (lane % LPR) * 8;
+      const int n = nw0 + c8;
+      const bool ncol = n < p.n_store;
+      const bool full = n + 8 <= p.n_store;
+      const bool rvec = full && p.resid && resid_vec8(p);
+      float sc[8], bias8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        sc[e] = n + e < p.n_store ? p.wscale[n + e] : 0.f;
+        bias8[e] = p.bias && n + e < p.n_store ? p.bias[n + e] : 0.f;
+      }
+      const bool ovec = full && out_vec8(p);
+#pragma unroll
+      for (int t = 0; t < NP; ++t) {
+        const int rr = t * RPI + lane / LPR;
+        const int m = mb + rr;
+        if (m >= p.M || !ncol) continue;
+        float rs[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        if (p.resid) load_resid8(p, m, n, rvec, rs);
+        const f32x4 a0 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c8);
+        const f32x4 a1 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + c8 + 4);
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (e < 4 ? a0[e] : a1[e - 4]) * sc[e] + bias8[e] + rs[e];
+        if (p.out_fp8)
+          store8_fp8(p, m, n, v);
+        else
+          store8(p, m, n, v, ovec);
+      }
+    } else {
+      // GEGLU over 64-column (value, gate) pair blocks, as gemm_frag_kernel
+      if constexpr (WN % 64 == 0) {
+        constexpr int LPR = WN / 16;
+        constexpr int RPI = 64 / LPR;
+        const int cq = (lane % LPR) * 8;
+        const int pb = cq / 32, c8 = cq % 32;
+        const int lc = pb * 64 + c8;
+        const int nv = nw0 + lc;
+        const int o = nw0 / 2 + cq;
+        float ba[8], bg[8], sa[8], sg[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bool in = o < p.n_store;
+          ba[e] = in && p.bias ? p.bias[nv + e] : 0.f;
+          bg[e] = in && p.bias ? p.bias[nv + 32 + e] : 0.f;
+          sa[e] = in ? p.wscale[nv + e] : 0.f;
+          sg[e] = in ? p.wscale[nv + 32 + e] : 0.f;
+        }
+        const bool vec8 = !p.out_f32 && o + 8 <= p.n_store && out_vec8(p);
+#pragma unroll
+        for (int t = 0; t < 32 / RPI; ++t) {
+          const int rr = t * RPI + lane / LPR;
+          const f32x4 a0 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc);
+          const f32x4 a1 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 4);
+          const f32x4 g0 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 32);
+          const f32x4 g1 = *reinterpret_cast<const f32x4*>(ep + rr * EPL + lc + 36);
+          const int m = mb + rr;
+          if (m >= p.M || o >= p.n_store) continue;
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = (a0[e] * sa[e] + ba[e]) * gelu_erf(g0[e] * sg[e] + bg[e]);
+            v[e + 4] = (a1[e] * sa[e + 4] + ba[e + 4]) * gelu_erf(g1[e] * sg[e + 4] + bg[e + 4]);
+          }
+          if (p.out_fp8) {
+            store8_fp8(p, m, o, v);
+          } else if (vec8) {
+            bf16x8 w;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) w[e] = static_cast<bf16>(v[e]);
+            *reinterpret_cast<bf16x8*>(static_cast<bf16*>(p.out) + (long long)m * p.ldo + o) = w;
+          } else {
+            store4<bf16>(p, m, o, v, p.n_store);
+            store4<bf16>(p, m, o + 4, v + 4, p.n_store);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int FN, int S, int WPE, bool SPLIT>
+void launch_fp8(const GemmParams& p, int nsplit, hipStream_t s) {
+  constexpr size_t lds = frag_lds_bytes<BM, FN, S, 4>();
+  static bool attr_set = false;
+  if (!attr_set) {
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_fp8_kernel<BM, FN, S, WPE, SPLIT>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+    attr_set = true;
+  }
+  const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, 32 * FN * 4);
+  hipLaunchKernelGGL((gemm_fp8_kernel<BM, FN, S, WPE, SPLIT>), dim3(mt * nt * nsplit), dim3(256), lds, s, p, mt, nt,
+                     nsplit);
+  DN_HIP(hipGetLastError());
+}
+
+template <int BM, int FN, int S, int WPE> void run_fp8(const GemmParams& p, int nsplit, hipStream_t s) {
+  if (p.raw_partial) {
+    launch_fp8<BM, FN, S, WPE, true>(p, nsplit, s);
+  } else if (nsplit > 1) {
+    launch_fp8<BM, FN, S, WPE, true>(p, nsplit, s);
+    // the slabs hold scaled sums; the reduction applies bias / residual (unit scales)
+    GemmParams q = p;
+    splitk_reduce(q, nsplit, s);
+  } else {
+    launch_fp8<BM, FN, S, WPE, false>(p, 1, s);
+  }
+}
+
 // Fragment order of a packed [N][K] weight matrix (N rounded up to 32, K % 16 == 0):
 // element (n, k) lives at ((n / 32) * (K / 16) + k / 16) * 512 + lane * 8 + k % 8 with
 // lane = n % 32 + 32 * ((k % 16) / 8).
@@ -745,6 +1077,43 @@ void to_frag(const bf16* src, int N, int K, int ld_src, bf16* dst, hipStream_t s
   const int blocks = static_cast<int>(std::min<long long>((nv + 255) / 256, 16384));
   hipLaunchKernelGGL(to_frag_kernel, dim3(std::max(blocks, 1)), dim3(256), 0, s, src, N, K, ld_src, dst, Npad);
   DN_HIP(hipGetLastError());
+}
+
+bool gemm_fp8_layout(int N, int K) { return N >= 32 && N % 32 == 0 && K >= 128 && K % 128 == 0; }
+
+size_t gemm_fp8_code_bytes(int N, int K) { return (size_t)((N + 31) / 32 * 32) * K; }
+
+GemmPlan gemm_plan_fp8(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce) {
+  // the bf16 planner's choice among its 128 x 256 and 128 x 128 tiles (and its split)
+  GemmPlan g = frag_plan(M, N, K, geglu, cus, allow_split, fused_reduce, false);
+  if (!(g.bm == 128 && (g.bn == 256 || g.bn == 128))) {
+    g.bm = 128;
+    g.bn = (geglu || N >= 1024) ? 256 : 128;
+    g.split = 1;
+  }
+  while (g.split > 1 && K / 128 < 2 * g.split) --g.split;
+  g.frag = 1;
+  g.stages = 3;
+  return g;
+}
+
+void gemm_fp8(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
+  DN_CHECK(gemm_fp8_layout(p.N, p.K), "gemm_fp8: N % 32 == 0 and K % 128 == 0 needed");
+  DN_CHECK(p.taps == 1 && p.c1 == 0 && p.c0 == p.K, "gemm_fp8: one linear A source");
+  DN_CHECK(p.a0 && p.b && p.out && p.wscale && p.zero16, "gemm_fp8: null operand");
+  DN_CHECK(p.lda0 % 16 == 0, "gemm_fp8: A rows must be 16-byte aligned");
+  DN_CHECK(!p.vt, "gemm_fp8: no V^T output");
+  DN_CHECK(g.split >= 1 && g.split <= kMaxSplit && p.K / 128 >= g.split, "gemm_fp8: bad split");
+  DN_CHECK(!p.geglu || g.bn == 256, "gemm_fp8: GEGLU needs 64-column value/gate pairs per wave");
+  if (g.split > 1 || p.raw_partial) {
+    DN_CHECK(!p.geglu && !p.out_fp8, "gemm_fp8: split-K takes neither GEGLU nor fp8 output");
+    DN_CHECK(p.n_store % 4 == 0 && p.n_store == p.N, "gemm_fp8: split-K needs n_store == N, a multiple of 4");
+    DN_CHECK(p.part && p.part_floats >= (size_t)g.split * p.M * p.n_store, "gemm_fp8: split-K workspace too small");
+  }
+  if (g.bn == 256)
+    run_fp8<128, 2, 3, 2>(p, g.split, s);
+  else
+    run_fp8<128, 1, 3, 2>(p, g.split, s);
 }
 
 void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {

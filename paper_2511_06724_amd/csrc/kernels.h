@@ -49,6 +49,10 @@ struct GemmParams {
   // Raw partial output: write the slabs (even unsplit) and skip the reduction and the
   // epilogue; a later kernel (layernorm_reduce) completes them.
   int raw_partial = 0;
+  // fp8 kernel (gemm_fp8): per-output-row fp32 weight scales (the accumulator of column n
+  // is multiplied by wscale[n]); out_fp8: the output is E4M3 codes.
+  const float* wscale = nullptr;
+  int out_fp8 = 0;
 };
 
 // Block tile (bm x bn) of one GEMM launch and the kernel that runs it.
@@ -66,11 +70,20 @@ template <typename T>
 GemmPlan gemm_plan(int M, int N, int K, int geglu, int cus, bool allow_split = true, bool fused_reduce = false,
                    bool conv = false);
 template <typename T> void gemm(const GemmParams& p, const GemmPlan& g, hipStream_t s);
+// The fragment-B kernel's tile plan (cost model fitted to measured SD-XL GEMM times).
+GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce, bool conv);
 void gemm_bf16_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s);
 // bf16 weight matrices [N][K] with gemm_frag_layout(N, K) are stored in MFMA fragment
 // order (gemm_frag.hip) and multiplied by the fragment-B kernel; every other shape,
 // and fp32, keeps the row-major [N][K] layout.
 bool gemm_frag_layout(int N, int K);
+// fp8 (E4M3) GEMM: A fp8 codes [M][lda], B a matrix packed by pack_fp8 (codes in the
+// fragment order of the 32x32x64 fp8 matrix-core step, fp32 row scales in p.wscale);
+// N % 32 == 0, K % 128 == 0. Tile plans 128 x 256 and 128 x 128, split-K as gemm_plan.
+GemmPlan gemm_plan_fp8(int M, int N, int K, int geglu, int cus, bool allow_split, bool fused_reduce);
+void gemm_fp8(const GemmParams& p, const GemmPlan& g, hipStream_t s);
+bool gemm_fp8_layout(int N, int K);
+size_t gemm_fp8_code_bytes(int N, int K);  // N rounded up to 32, times K
 size_t gemm_frag_elems(int N, int K);  // N rounded up to 32, times K
 void to_frag(const bf16* src, int N, int K, int ld_src, bf16* dst, hipStream_t s);
 // fp32 workspace floats the plan needs (split-K partial slabs), 0 when none.
@@ -158,6 +171,11 @@ struct PackParams {
   int frag = 0;                    // 1: write dst in fragment order (gemm_frag.hip; ld_dst unused)
 };
 template <typename T> void pack(const PackParams& p, hipStream_t s);
+// E4M3 quantisation of a [rows][cols] fp32 source (the same row mapping as pack; column
+// mode 0 only): per destination row r, scale[r] = max_c |src| / 448 (1 for a zero row)
+// and code = round(src / scale) (nearest even, saturating), written in the fp8
+// fragment order to p.dst (bytes); rows past the source (up to a multiple of 32) are zero.
+void pack_fp8(const PackParams& p, float* scales, hipStream_t s);
 void pack_bias(float* dst, int n, const float* src, int src_n, int row_mode, int D, int Dp, hipStream_t s);
 
 // ---------------------------------------------------------------- cache lookup

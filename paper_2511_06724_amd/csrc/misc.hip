@@ -180,6 +180,35 @@ template <typename T> __global__ void pack_kernel(PackParams p) {
   }
 }
 
+// One workgroup per destination row r of the fp8 matrix: the row's largest magnitude,
+// its scale, then every code at its fragment position (see pack_fp8 in kernels.h):
+// byte ((r / 32) * (cols / 64) + c / 64) * 2048 + (r % 32 + 32 * ((c % 64) / 32)) * 32 + c % 32.
+__global__ __launch_bounds__(256) void pack_fp8_kernel(PackParams p, float* scales, int rows_pad) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const long long sr = r < p.rows ? pack_src_row(p, r) : -1;
+  const float* src = sr >= 0 ? p.src + sr * p.src_cols : nullptr;
+  float m = 0.f;
+  if (src)
+    for (int c = threadIdx.x; c < p.src_cols; c += 256) m = fmaxf(m, fabsf(src[c]));
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const float s = m > 0.f ? m / 448.f : 1.f;  // IEEE division, as the scale is defined
+  if (threadIdx.x == 0) scales[r] = s;
+  uint8_t* dst = static_cast<uint8_t*>(p.dst);
+  const long long kst = p.cols / 64;
+  for (int c4 = threadIdx.x * 4; c4 < p.cols; c4 += 1024) {
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (src)
+      for (int e = 0; e < 4; ++e)
+        if (c4 + e < p.src_cols) v[e] = src[c4 + e] / s;
+    const long long o = ((long long)(r >> 5) * kst + c4 / 64) * 2048 + ((r & 31) + 32 * ((c4 & 63) >> 5)) * 32 + (c4 & 31);
+    *reinterpret_cast<unsigned*>(dst + o) = fp8x4(v[0], v[1], v[2], v[3]);
+  }
+}
+
 __global__ void pack_bias_kernel(float* dst, int n, const float* src, int src_n, int row_mode, int D, int Dp) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= n) return;
@@ -250,6 +279,13 @@ void bf16_latent_to_f32(const uint16_t* src, float* dst, long long n, hipStream_
 
 template <typename T> void pack(const PackParams& p, hipStream_t s) {
   hipLaunchKernelGGL(pack_kernel<T>, dim3(blocks_for((long long)p.rows * p.cols)), dim3(256), 0, s, p);
+  DN_HIP(hipGetLastError());
+}
+
+void pack_fp8(const PackParams& p, float* scales, hipStream_t s) {
+  DN_CHECK(p.col_mode == 0 && p.cols % 128 == 0 && p.src_cols <= p.cols, "pack_fp8: columns must be a multiple of 128");
+  const int rows_pad = (p.rows + 31) / 32 * 32;
+  hipLaunchKernelGGL(pack_fp8_kernel, dim3(rows_pad), dim3(256), 0, s, p, scales, rows_pad);
   DN_HIP(hipGetLastError());
 }
 

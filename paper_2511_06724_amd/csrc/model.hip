@@ -146,7 +146,8 @@ struct TableBuilder {
 
 void validate_config(const dn_config& c) {
   DN_CHECK(c.abi_version == DN_ABI_VERSION, "config: abi_version mismatch");
-  DN_CHECK(c.dtype == DN_FP32 || c.dtype == DN_BF16, "config: dtype must be DN_FP32 or DN_BF16");
+  DN_CHECK(c.dtype == DN_FP32 || c.dtype == DN_BF16 || c.dtype == DN_FP8,
+           "config: dtype must be DN_FP32, DN_BF16 or DN_FP8");
   DN_CHECK(c.batch >= 1 && c.batch <= 64, "config: batch must be in [1, 64]");
   DN_CHECK(c.latent_c >= 1 && c.latent_c <= kCinPad, "config: latent_c must be in [1, 64]");
   DN_CHECK(c.n_levels >= 1 && c.n_levels <= DN_MAX_LEVELS, "config: n_levels must be in [1, 4]");
@@ -176,6 +177,8 @@ void validate_config(const dn_config& c) {
     DN_CHECK(lv.channels % c.gn_groups == 0, "config: level channels not divisible by gn_groups");
     DN_CHECK(lv.depth >= 0 && lv.depth <= 64, "config: level depth must be in [0, 64]");
     const bool attn = lv.depth > 0 || (l == c.n_levels - 1 && c.mid_depth > 0);
+    if (c.dtype == DN_FP8 && (lv.depth > 0 || (l == c.n_levels - 1 && c.mid_depth > 0)))
+      DN_CHECK(lv.channels % 128 == 0, "config: DN_FP8 needs transformer widths that are multiples of 128");
     if (attn) {
       DN_CHECK(lv.heads >= 1 && lv.head_dim >= 1 && lv.head_dim <= 64, "config: heads >= 1, head_dim in [1, 64]");
       DN_CHECK(lv.heads * lv.head_dim == lv.channels, "config: heads * head_dim must equal channels");
@@ -255,6 +258,7 @@ struct ConvW {
 struct LinW {
   void* w = nullptr;  // [n][k]
   float* b = nullptr;
+  float* scale = nullptr;  // fp8 matrices: per-row scales (w then holds E4M3 codes)
   int n = 0, k = 0;
 };
 struct Norm {
@@ -292,6 +296,7 @@ struct Model {
   int n = 0;         // UNet batch = 2B
   size_t esz = 2;    // element size of activations / packed weights
   bool bf = true;
+  bool fp8ff = false;  // the GEGLU feed-forward on E4M3 operands (dtype DN_FP8)
   int temb_dim = 0, temb_total = 0;
   // parameters
   void* packed = nullptr;  // all packed weight matrices
@@ -409,6 +414,30 @@ struct Packer {
     return l;
   }
   Norm norm(const std::string& n) { return Norm{copy_param(n + ".g"), copy_param(n + ".b")}; }
+  // fp8 (E4M3) matrix: codes in the fp8 fragment order and one scale per row (no bias);
+  // row_mode 1 interleaves the GEGLU value / gate rows as pack_mat does
+  LinW lin_fp8(const std::string& n, int rows, int cols, int row_mode) {
+    LinW l;
+    l.n = rows;
+    l.k = cols;
+    const size_t bytes = gemm_fp8_code_bytes(rows, cols);
+    l.w = alloc_packed((bytes + m->esz - 1) / m->esz);
+    l.scale = alloc_params((rows + 31) / 32 * 32);
+    if (!dry) {
+      PackParams p;
+      p.dst = l.w;
+      p.rows = rows;
+      p.cols = cols;
+      p.ld_dst = cols;
+      p.src = blob + t(n + ".w").offset;
+      p.row_mode = row_mode;
+      p.col_mode = 0;
+      p.src_rows = rows;
+      p.src_cols = cols;
+      pack_fp8(p, l.scale, s);
+    }
+    return l;
+  }
 };
 
 void build(Model* m, Packer& pk, const dn_config& cfg, const std::vector<Walker::Ev>& ev) {
@@ -507,11 +536,20 @@ void build(Model* m, Packer& pk, const dn_config& cfg, const std::vector<Walker:
           tb.ln3 = pk.norm(b + ".ln3");
           tb.ff1.n = 2 * F * C;
           tb.ff1.k = C;
-          tb.ff1.w = pk.alloc_packed((size_t)2 * F * C * C);
-          pk.pack_mat(tb.ff1.w, 2 * F * C, C, C, pk.t(b + ".ff1.w"), 1, 0, 2 * F * C, C);
+          if (m->fp8ff) {
+            tb.ff1 = pk.lin_fp8(b + ".ff1", 2 * F * C, C, 1);
+          } else {
+            tb.ff1.w = pk.alloc_packed((size_t)2 * F * C * C);
+            pk.pack_mat(tb.ff1.w, 2 * F * C, C, C, pk.t(b + ".ff1.w"), 1, 0, 2 * F * C, C);
+          }
           tb.ff1.b = pk.alloc_params(2 * F * C);
           if (!pk.dry) pack_bias(tb.ff1.b, 2 * F * C, pk.blob + pk.t(b + ".ff1.b").offset, 2 * F * C, 1, 0, 0, pk.s);
-          tb.ff2 = pk.lin(b + ".ff2", C, F * C, true);
+          if (m->fp8ff) {
+            tb.ff2 = pk.lin_fp8(b + ".ff2", C, F * C, 0);
+            tb.ff2.b = pk.copy_param(b + ".ff2.b");
+          } else {
+            tb.ff2 = pk.lin(b + ".ff2", C, F * C, true);
+          }
           tb.kv_slot = m->n_kv_slots++;
           x.blocks.push_back(tb);
         }
@@ -653,7 +691,8 @@ Model* model_create(const dn_config& cfg, const float* weights, size_t n_floats,
   std::unique_ptr<Model> m(new Model());
   m->cfg = cfg;
   m->n = 2 * cfg.batch;
-  m->bf = cfg.dtype == DN_BF16;
+  m->bf = cfg.dtype != DN_FP32;
+  m->fp8ff = cfg.dtype == DN_FP8;
   m->esz = m->bf ? 2 : 4;
   m->temb_dim = 4 * cfg.model_channels;
   const auto ev = walk(cfg);
@@ -773,7 +812,8 @@ template <typename T> struct Exec {
   size_t split_need = 0;  // dry walk: largest split-K workspace (floats) of the step
 
   void run_gemm(GemmParams& p) {
-    const GemmPlan g = gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus, p.vt == nullptr, false, p.taps == 9);
+    const GemmPlan g = p.wscale ? gemm_plan_fp8(p.M, p.N, p.K, p.geglu, m->cus, true, false)
+                                : gemm_plan<T>(p.M, p.N, p.K, p.geglu, m->cus, p.vt == nullptr, false, p.taps == 9);
     if (dry) {
       split_need = std::max(split_need, gemm_workspace_floats(g, p.M, p.N));
       return;
@@ -781,7 +821,10 @@ template <typename T> struct Exec {
     p.zero16 = m->zero;
     p.part = m->split_ws;
     p.part_floats = m->split_floats;
-    gemm<T>(p, g, s);
+    if (p.wscale)
+      gemm_fp8(p, g, s);
+    else
+      gemm<T>(p, g, s);
   }
 
   void conv(const ConvW& w, const void* x, int in_h, int in_w, int up, int stride, void* out, int out_h, int out_w,
@@ -853,6 +896,8 @@ template <typename T> struct Exec {
     p.vt_heads = vt.heads;
     p.vt_seq = vt.seq;
     p.vt_ld = vt.ld;
+    p.wscale = w.scale;
+    p.out_fp8 = w.scale && geglu;  // the fp8 feed-forward's hidden layer stays in E4M3
     run_gemm(p);
   }
 
@@ -922,7 +967,8 @@ template <typename T> struct Exec {
     bool resid = true;
   };
   Pending residual_gemm(const LinW& w, const void* x, int ldx, long long M, bool resid) {
-    const GemmPlan g = gemm_plan<T>(static_cast<int>(M), w.n, w.k, 0, m->cus, true, true);
+    const GemmPlan g = w.scale ? gemm_plan_fp8(static_cast<int>(M), w.n, w.k, 0, m->cus, true, true)
+                               : gemm_plan<T>(static_cast<int>(M), w.n, w.k, 0, m->cus, true, true);
     if (!g.frag || g.split == 1) {
       linear(w, x, ldx, M, m->R, w.n, true, resid ? m->R : nullptr, w.n, true);
       return Pending{};
@@ -942,18 +988,31 @@ template <typename T> struct Exec {
     p.out_f32 = 1;
     p.n_store = w.n;
     p.raw_partial = 1;
+    p.wscale = w.scale;
     if (dry) {
       split_need = std::max(split_need, gemm_workspace_floats(g, p.M, p.N, true));
     } else {
       p.zero16 = m->zero;
       p.part = m->split_ws;
       p.part_floats = m->split_floats;
-      gemm<T>(p, g, s);
+      if (w.scale)
+        gemm_fp8(p, g, s);
+      else
+        gemm<T>(p, g, s);
     }
     return Pending{&w, g.split, resid};
   }
-  void ln_after(const Pending& pd, long long M, int C, const Norm& nm) {
+  // fp8: the LayerNorm feeding the fp8 feed-forward writes E4M3 codes
+  void ln_after(const Pending& pd, long long M, int C, const Norm& nm, bool fp8 = false) {
     if (dry) return;
+    if (fp8) {
+      if (pd.nsplit)
+        layernorm_reduce<uint8_t>(m->R, P_<uint8_t>(m->a), M, C, nm.g, nm.b, m->cfg.ln_eps, m->split_ws, pd.nsplit,
+                                  pd.w->b, pd.resid, s);
+      else
+        layernorm<uint8_t>(m->R, P_<uint8_t>(m->a), M, C, nm.g, nm.b, m->cfg.ln_eps, s);
+      return;
+    }
     if (pd.nsplit)
       layernorm_reduce<T>(m->R, P_<T>(m->a), M, C, nm.g, nm.b, m->cfg.ln_eps, m->split_ws, pd.nsplit, pd.w->b,
                           pd.resid, s);
@@ -992,7 +1051,7 @@ template <typename T> struct Exec {
       attention_(m->q2, P, (long long)HW * P, kv, P, (long long)m->cfg.ctx_len * P, vtc,
                  (m->cfg.ctx_len + 63) / 64 * 64, HW, m->cfg.ctx_len, x);
       pd = residual_gemm(b.o2, m->o, P, M, true);
-      ln_after(pd, M, C, b.ln3);
+      ln_after(pd, M, C, b.ln3, m->fp8ff);
       linear(b.ff1, m->a, C, M, m->ff, m->cfg.ff_mult * C, false, nullptr, 0, false, true);
       if (!last)
         pd = residual_gemm(b.ff2, m->ff, m->cfg.ff_mult * C, M, true);

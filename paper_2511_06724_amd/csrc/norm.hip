@@ -236,6 +236,11 @@ __global__ __launch_bounds__(256) void gn_apply_kernel(GroupNormParams p, GnGeom
 constexpr int kLnMaxVec = 8;  // float4 vectors per lane: C <= 2048
 
 template <typename T> struct Store4;
+template <> struct Store4<uint8_t> {  // E4M3 codes
+  __device__ static __forceinline__ void st(uint8_t* p, float a, float b, float c, float d) {
+    *reinterpret_cast<unsigned*>(p) = fp8x4(a, b, c, d);
+  }
+};
 template <> struct Store4<bf16> {
   __device__ static __forceinline__ void st(bf16* p, float a, float b, float c, float d) {
     bf16x4 o;
@@ -425,5 +430,9 @@ template void layernorm_reduce<float>(float*, float*, long long, int, const floa
                                       int, const float*, bool, hipStream_t);
 template void layernorm_reduce<bf16>(float*, bf16*, long long, int, const float*, const float*, float, const float*,
                                      int, const float*, bool, hipStream_t);
+template void layernorm_reduce<uint8_t>(float*, uint8_t*, long long, int, const float*, const float*, float,
+                                        const float*, int, const float*, bool, hipStream_t);
+template void layernorm<uint8_t>(const float*, uint8_t*, long long, int, const float*, const float*, float,
+                                 hipStream_t);
 
 }  // namespace dn

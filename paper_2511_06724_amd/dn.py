@@ -16,7 +16,7 @@ from .workloads import DnConfig, VaeConfig
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libargus_dn.so")
 
 DN_OK, DN_EINVAL, DN_ENOMEM, DN_EHIP, DN_EUNSUPPORTED = 0, -1, -2, -3, -4
-DN_FP32, DN_BF16 = 0, 1
+DN_FP32, DN_BF16, DN_FP8 = 0, 1, 2
 DN_WEIGHTS_HOST, DN_WEIGHTS_DEVICE = 0, 1
 ABI_VERSION = 1
 MAX_LEVELS = 4
@@ -369,9 +369,11 @@ def packed_weight_elems(dtype, N, K):
 
 
 def pack_weight(dtype, w, N, K, stream=None):
-    """Row-major device weight [N][K] (dtype elements) -> a new tensor in the GEMM's packed layout."""
+    """Row-major device weight [N][K] (dtype elements; fp32 for DN_FP8) -> a new tensor in
+    the GEMM's packed layout (for DN_FP8 a uint8 tensor: codes, then N fp32 scales)."""
     import torch
-    out = torch.empty(packed_weight_elems(dtype, N, K), device=w.device, dtype=w.dtype)
+    out = torch.empty(packed_weight_elems(dtype, N, K), device=w.device,
+                      dtype=torch.uint8 if dtype == DN_FP8 else w.dtype)
     _check(lib.dn_pack_weight(dtype, _ptr(w), N, K, _ptr(out), _stream(stream)))
     return out
 

@@ -17,6 +17,7 @@ import numpy as np
 
 DN_FP32 = 0
 DN_BF16 = 1
+DN_FP8 = 2
 
 
 @dataclass

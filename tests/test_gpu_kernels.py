@@ -380,3 +380,100 @@ def test_sdxl_linear_shapes_sampled_and_deterministic(M, N, K):
     for m, n in zip(*_sample_idx(r, (M, N), 400)):
         ref = float(xh[m] @ wh[n] + bh[n] + rh[m, n])
         assert abs(yh[m, n] - ref) <= 2e-3 * max(1.0, abs(ref)), (m, n, yh[m, n], ref)
+
+
+# ----------------------------------------------------------------------------- fp8 (E4M3) quantized variant
+
+def _fp8_offsets(N, K):
+    """Byte offset of (n, k) in the fp8 fragment order (pack_fp8)."""
+    n = np.arange(N)[:, None]
+    k = np.arange(K)[None, :]
+    return ((n // 32) * (K // 64) + k // 64) * 2048 + ((n % 32) + 32 * ((k % 64) // 32)) * 32 + (k % 32)
+
+
+def _fp8_values(codes_u8):
+    return torch.from_numpy(np.ascontiguousarray(codes_u8)).view(torch.float8_e4m3fn).float().numpy()
+
+
+def _to_fp8_dev(x):
+    """fp32 values -> (device E4M3 codes, the values they hold)."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.float8_e4m3fn)
+    return t.view(torch.uint8).to(DEV), t.float().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("N,K", [(64, 128), (1280, 5120), (640, 256)])
+def test_fp8_pack_matches_oracle_quantization(N, K):
+    """dn_pack_weight(DN_FP8): every row scale bitwise the oracle's, every code the
+    oracle's quantised value."""
+    from oracle import quant as Q
+    announce(f"fp8 pack N={N} K={K}")
+    r = _rng(N + K)
+    w = (r.standard_normal((N, K)) * r.uniform(0.01, 2.0, (N, 1))).astype(np.float32)
+    w[3] = 0.0
+    packed = dn.pack_weight(dn.DN_FP8, torch.from_numpy(w).to(DEV), N, K).cpu().numpy()
+    scales = packed[N * K:].view(np.float32)
+    deq, s = Q.quantize_rows(w)
+    assert np.array_equal(scales.view(np.uint32), s.view(np.uint32))
+    vals = _fp8_values(packed[:N * K][_fp8_offsets(N, K)])
+    assert np.array_equal((vals * s[:, None]).astype(np.float32), deq)
+
+
+@pytest.mark.parametrize("M,N,K,geglu,resid", [(300, 256, 256, False, False), (2048, 1280, 5120, False, True),
+                                               (1000, 640, 1280, False, True), (300, 256, 128, True, False),
+                                               (2048, 5120, 1280, True, False)])
+def test_fp8_linear(M, N, K, geglu, resid):
+    """The fp8 GEMM against the oracle on the quantised operands: fp32 output within
+    1e-5 (products exact, fp32 sums in another order); the GEGLU output in E4M3 against
+    the oracle's E4M3 rounding of the exact result (at least 99 % identical codes, the
+    rest one quantum off at rounding boundaries)."""
+    from oracle import quant as Q
+    announce(f"fp8 linear M={M} N={N} K={K} geglu={geglu} resid={resid}")
+    r = _rng(3 * M + N + K)
+    Nw = 2 * N if geglu else N
+    x8, xh = _to_fp8_dev(r.standard_normal((M, K)))
+    w = (r.standard_normal((Nw, K)) / math.sqrt(K)).astype(np.float32)
+    b = r.standard_normal(Nw).astype(np.float32)
+    wi = _interleave(w, N) if geglu else w
+    bi = _interleave(b[:, None], N)[:, 0].copy() if geglu else b
+    wp = dn.pack_weight(dn.DN_FP8, torch.from_numpy(wi).to(DEV), Nw, K)
+    wq = Q.quantize_rows(w)[0].astype(np.float64)      # the same quantisation row by row
+    u = xh @ wq.T + b.astype(np.float64)
+    if geglu:
+        y = torch.empty((M, N), device=DEV, dtype=torch.uint8)
+        dn.op_linear(dn.DN_FP8, x8, wp, f32_dev(bi), y, M, N, K, geglu=True)
+        torch.cuda.synchronize()
+        ref = u[:, :N] * L.gelu(u[:, N:])
+        got = _fp8_values(y.cpu().numpy())
+        want = Q.fp8_round(ref)
+        assert rel_l2(got, ref) < 4e-2
+        assert np.mean(got == want) >= 0.99
+        return
+    res = r.standard_normal((M, N)).astype(np.float32) if resid else None
+    y = torch.empty((M, N), device=DEV)
+    dn.op_linear(dn.DN_FP8, x8, wp, f32_dev(b), y, M, N, K, resid=f32_dev(res) if resid else None, resid_f32=True,
+                 y_f32=True)
+    yb = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+    dn.op_linear(dn.DN_FP8, x8, wp, f32_dev(b), yb, M, N, K)
+    torch.cuda.synchronize()
+    ref = u + (res if resid else 0.0)
+    assert rel_l2(host(y), ref) < 1e-5
+    assert rel_l2(host(yb), u) < 8e-3
+
+
+def test_fp8_layernorm():
+    """LayerNorm with E4M3 output: codes identical to the oracle's rounding of the exact
+    normalised values except at rounding boundaries."""
+    from oracle import quant as Q
+    announce("fp8 layernorm 2048x1280")
+    M, C = 2048, 1280
+    r = _rng(99)
+    x = (1.0 + 3.0 * r.standard_normal((M, C))).astype(np.float32)
+    g = (1 + 0.1 * r.standard_normal(C)).astype(np.float32)
+    b = (0.1 * r.standard_normal(C)).astype(np.float32)
+    y = torch.empty((M, C), device=DEV, dtype=torch.uint8)
+    dn.op_layernorm(dn.DN_FP8, f32_dev(x), y, M, C, f32_dev(g), f32_dev(b), 1e-5)
+    torch.cuda.synchronize()
+    ref = L.layer_norm(x.astype(np.float64), g.astype(np.float64), b.astype(np.float64), 1e-5)
+    got = _fp8_values(y.cpu().numpy())
+    assert np.mean(got == Q.fp8_round(ref)) >= 0.999
+    assert rel_l2(got, ref) < 4e-2
