@@ -24,6 +24,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
@@ -104,29 +105,40 @@ def unet_flops(cfg, n):
 
 
 # Single-GEMM workloads of the 32x32 SD-XL transformer blocks (M = 2048 tokens at batch 2
-# with guidance): name -> (M, N outputs, K, GEGLU, fp32 residual + fp32 output).
+# with guidance): name -> (M, N outputs, K, GEGLU, fp32 residual + fp32 output, fp8).
+# The fp8 cases are the quantized variant's feed-forward (E4M3 operands; FF-in writes
+# E4M3 GEGLU outputs).
 GEMM_CASES = {
-    "ffin": (2048, 5120, 1280, True, False),    # FF-in, 2 x 5120 packed columns -> 5120 GEGLU outputs
-    "proj": (2048, 1280, 1280, False, True),    # attention out-projection into the fp32 residual stream
-    "qkv": (2048, 3840, 1280, False, False),    # fused Q, K, V projection (bf16 output)
-    "ffout": (2048, 1280, 5120, False, True),   # FF-out into the fp32 residual stream
+    "ffin": (2048, 5120, 1280, True, False, False),    # FF-in, 2 x 5120 packed columns -> 5120 GEGLU outputs
+    "proj": (2048, 1280, 1280, False, True, False),    # attention out-projection into the fp32 residual stream
+    "qkv": (2048, 3840, 1280, False, False, False),    # fused Q, K, V projection (bf16 output)
+    "ffout": (2048, 1280, 5120, False, True, False),   # FF-out into the fp32 residual stream
+    "ffin8": (2048, 5120, 1280, True, False, True),    # FF-in of the quantized variant
+    "ffout8": (2048, 1280, 5120, False, True, True),   # FF-out of the quantized variant
 }
 
 
 def gemm_case(torch, dn, name, stream):
     """Operands of one GEMM case and a function that launches it once on `stream`."""
-    M, N, K, geglu, resid = GEMM_CASES[name]
+    M, N, K, geglu, resid, fp8 = GEMM_CASES[name]
     Nw = 2 * N if geglu else N
-    x = torch.randn((M, K), device="cuda").to(torch.bfloat16)
-    w = (torch.randn((Nw, K), device="cuda") / math.sqrt(K)).to(torch.bfloat16)
+    dt = dn.DN_FP8 if fp8 else dn.DN_BF16
+    if fp8:
+        x = torch.randn((M, K), device="cuda").to(torch.float8_e4m3fn).view(torch.uint8)
+        w = torch.randn((Nw, K), device="cuda") / math.sqrt(K)
+        ydt = torch.float32 if resid else torch.uint8
+    else:
+        x = torch.randn((M, K), device="cuda").to(torch.bfloat16)
+        w = (torch.randn((Nw, K), device="cuda") / math.sqrt(K)).to(torch.bfloat16)
+        ydt = torch.float32 if resid else torch.bfloat16
     b = torch.randn(Nw, device="cuda")
     r = torch.randn((M, N), device="cuda") if resid else None
-    y = torch.empty((M, N), device="cuda", dtype=torch.float32 if resid else torch.bfloat16)
-    w = dn.pack_weight(dn.DN_BF16, w, Nw, K)
+    y = torch.empty((M, N), device="cuda", dtype=ydt)
+    w = dn.pack_weight(dt, w, Nw, K)
 
     class Launch:
         def __call__(self):
-            dn.op_linear(dn.DN_BF16, x, w, b, y, M, N, K, resid=r, resid_f32=resid, y_f32=resid, geglu=geglu,
+            dn.op_linear(dt, x, w, b, y, M, N, K, resid=r, resid_f32=resid, y_f32=resid, geglu=geglu,
                          stream=stream)
 
         def rewarm_input(self):
@@ -136,14 +148,13 @@ def gemm_case(torch, dn, name, stream):
     return Launch(), 2.0 * M * Nw * K
 
 
-def roofline_ff_in(torch, dn, stream, iters=20):
-    """FF-in GEGLU GEMM of a 32x32 SD-XL transformer block: M = 2048 tokens (batch 2),
-    K = 1280, 2 x 5120 packed output columns -> 5120 GEGLU outputs. Each launch is timed
-    alone with HIP events on the library's stream, after a 1 GiB read has evicted the
-    caches (in the denoise step every layer's weights come from HBM; the activations it
-    reads were just written, so they are re-read into the caches here too); the
-    back-to-back time with the weights cache-resident is reported beside it."""
-    launch, flops = gemm_case(torch, dn, "ffin", stream)
+def time_gemm(torch, dn, name, stream, iters=20):
+    """(FLOPs per launch, mean seconds per launch with the caches evicted before each, mean
+    seconds back to back). Each launch is timed alone with HIP events on the library's
+    stream, after a 1 GiB read has evicted the caches (in the denoise step every layer's
+    weights come from HBM; the activations it reads were just written, so they are
+    re-read into the caches here too)."""
+    launch, flops = gemm_case(torch, dn, name, stream)
     flush = torch.empty(256 << 20, device="cuda", dtype=torch.float32).fill_(1.0)
     for _ in range(3):
         launch()
@@ -165,7 +176,14 @@ def roofline_ff_in(torch, dn, stream, iters=20):
     torch.cuda.synchronize()
     warm_s = sum(e0.elapsed_time(e1) for e0, e1 in ev) / 1e3 / iters
     del flush
-    avg_s = sum(cold) / len(cold)
+    return flops, sum(cold) / len(cold), warm_s
+
+
+def roofline_ff_in(torch, dn, stream, iters=20):
+    """FF-in GEGLU GEMM of a 32x32 SD-XL transformer block: M = 2048 tokens (batch 2),
+    K = 1280, 2 x 5120 packed output columns -> 5120 GEGLU outputs, timed as time_gemm
+    does; the back-to-back time with the weights cache-resident is reported beside it."""
+    flops, avg_s, warm_s = time_gemm(torch, dn, "ffin", stream, iters)
     achieved = flops / avg_s / 1e12
     return {"kernel": "gemm_frag_kernel<bf16,128x256> FF-in GEGLU 2048x10240x1280", "bound": "mfma",
             "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -175,6 +193,30 @@ def roofline_ff_in(torch, dn, stream, iters=20):
             "warm_avg_launch_us": round(warm_s * 1e6, 2),
             "warm_frac": round(flops / warm_s / 1e12 / PEAK_BF16_TFLOPS, 4),
             "kernel_source_hash": kernel_source_hash()}
+
+
+def fp8_feed_forward(torch, dn, stream):
+    """The quantized variant's two feed-forward GEMMs at the 32x32 SD-XL block shape against
+    the fp8 peak, beside the bf16 ones."""
+    out = {}
+    for name in ("ffin8", "ffout8", "ffout"):
+        flops, cold, warm = time_gemm(torch, dn, name, stream)
+        peak = PEAK_FP8_TFLOPS if GEMM_CASES[name][5] else PEAK_BF16_TFLOPS
+        out[name] = {"avg_launch_us": round(cold * 1e6, 2), "warm_avg_launch_us": round(warm * 1e6, 2),
+                     "achieved_tflops": round(flops / cold / 1e12, 1), "peak": peak,
+                     "frac": round(flops / cold / 1e12 / peak, 4)}
+    return out
+
+
+def fp8_variant(torch, dn, W, images=2):
+    """The quantized variant (E4M3 feed-forward) of the SD-XL UNet: 50 steps with guidance."""
+    cfg = W.sdxl(W.DN_FP8)
+    model = model_for(torch, dn, cfg)
+    sec = time_images(torch, model, cfg, ts50(), images=images, warmup=1)
+    model.close()
+    torch.cuda.empty_cache()
+    return {"workload": "SD-XL-shaped UNet, E4M3 GEGLU feed-forward, bf16 elsewhere, 50 steps, CFG",
+            "denoise_steps_per_s": round(50 / sec, 3), "images_per_s": round(1 / sec, 4)}
 
 
 def profile_kernel(torch, dn, name):
@@ -580,6 +622,10 @@ def main():
         print(f"[bench] decoder {extra['vae_decode']['ms_per_decode']} ms per 1024x1024 image",
               file=sys.stderr, flush=True)
         extra["sd15_level"] = sd15_steps(torch, dn, W)
+        extra["fp8_variant"] = fp8_variant(torch, dn, W)
+        extra["fp8_variant"]["feed_forward_gemms"] = fp8_feed_forward(torch, dn, stream)
+        print(f"[bench] fp8 variant {extra['fp8_variant']['denoise_steps_per_s']} denoise steps/s",
+              file=sys.stderr, flush=True)
         extra["batch_variant_sweep"] = sweep_batch(torch, dn, W)
     cpu = None if args.no_cpu_baseline else cpu_baseline()
     out = {

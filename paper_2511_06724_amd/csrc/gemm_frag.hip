@@ -158,7 +158,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   constexpr int PW = BM / 32;  // DMA instructions (8 rows of 128 B) per DMA wave per stage
   static_assert(NW == 4 || NW == 5, "four or five waves");
   constexpr int NM = FM * FN;
-  static_assert(D == 1 || D == 2, "one or two B buffers");
+  static_assert(D >= 1 && D <= 3 && (!PRE || D <= 2), "one to three B buffers (two with read-ahead)");
   static_assert(S >= 2 && S <= 6, "2 to 6 LDS stages");
   static_assert(BM % 32 == 0 && BM <= 256, "BM");
 
@@ -301,7 +301,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   constexpr int ELPR = WN / 8;     // lanes per row in the row-contiguous epilogue
   constexpr int ERPI = 64 / ELPR;  // rows per pass
   constexpr int ENP = 32 / ERPI;   // passes per 32-row block
-  constexpr bool kPreIn = !SPLIT && !PRE && MODE != 2 && FM * ENP * 8 <= 32;
+  constexpr bool kPreIn = !SPLIT && !PRE && MODE != 2 && FM * ENP * 8 <= 32 && WPE <= 2;
   const int enw0 = n0 + wave * WN;
   const bool pre_in = kPreIn && !p.geglu && !(p.vt && enw0 + WN > p.vt_col0) &&
                       ((p.resid != nullptr) != (p.rowvec != nullptr));
@@ -460,7 +460,17 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
       kstep(std::true_type{}, kt + S, slot, nslot, 0, fa[1], fa[0], bb[3], kt + D, 3, bb);
     };
 
-    if constexpr (D == 2) {
+    if constexpr (D == 3) {
+      // Triples of stages, then the rest (as for pairs below)
+      int kt = kt0;
+      for (; kt + 2 < kt1; kt += 3) {
+        stage(kt, bq[0]);
+        stage(kt + 1, bq[1]);
+        stage(kt + 2, bq[2]);
+      }
+      if (kt < kt1) stage(kt, bq[0]);
+      if (kt + 1 < kt1) stage(kt + 1, bq[1]);
+    } else if constexpr (D == 2) {
       // Pairs of stages, then the odd one: no stage of the loop body is conditional, so
       // the compiler's wait for a B register counts both stages' loads issued after it.
       int kt = kt0;
@@ -705,7 +715,14 @@ void run_frag(const GemmParams& p, int nsplit, hipStream_t s) {
 // 64 x 160 and 128 x 160 (five waves) with two B buffers, one workgroup per CU.
 // stages = 2 selects the 128 x 256 variant with two B buffers and one workgroup per CU.
 template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
-  if (g.bm == 128 && g.bn == 256 && g.stages == 3) return run_frag<128, 2, 3, 1, 2, MODE>(p, g.split, s);
+  if (g.bm == 128 && g.bn == 256 && g.stages == 3) {
+    // B two stages ahead where the registers allow it (the implicit convolution's
+    // address registers do not leave room)
+    if constexpr (MODE == 2)
+      return run_frag<128, 2, 3, 1, 2, MODE>(p, g.split, s);
+    else
+      return run_frag<128, 2, 3, 2, 2, MODE>(p, g.split, s);
+  }
   if (g.bm == 128 && g.bn == 256 && g.stages == 2) return run_frag<128, 2, 3, 2, 1, MODE>(p, g.split, s);
   if (g.bm == 128 && g.bn == 128 && g.stages == 3) return run_frag<128, 1, 3, 2, 2, MODE>(p, g.split, s);
   if (g.bm == 64 && g.bn == 128 && g.stages == 3) return run_frag<64, 1, 3, 2, 4, MODE>(p, g.split, s);
@@ -715,9 +732,9 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   if (g.bm == 64 && g.bn == 256 && g.stages == 13) return run_frag<64, 2, 3, 2, 2, MODE, 1>(p, g.split, s);
   if (g.bm == 32 && g.bn == 128 && g.stages == 13) return run_frag<32, 1, 3, 2, 4, MODE, 1>(p, g.split, s);
   if constexpr (MODE != 2) {
-    if (g.bm == 64 && g.bn == 160 && g.stages == 3) return run_frag<64, 1, 3, 2, 2, MODE, 0, 5>(p, g.split, s);
+    if (g.bm == 64 && g.bn == 160 && g.stages == 3) return run_frag<64, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
   }
-  if (g.bm == 128 && g.bn == 160 && g.stages == 3) return run_frag<128, 1, 3, 2, 2, MODE, 0, 5>(p, g.split, s);
+  if (g.bm == 128 && g.bn == 160 && g.stages == 3) return run_frag<128, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
   throw Error(-1, "gemm: no fragment-B kernel for this tile plan");
 }
 
@@ -856,35 +873,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
                                                                     0, 127, 0, 127);
   };
 
-  // Prologue: A stages kt0 .. kt0 + 1, then B of step 2 kt0. Stage kt (r = kt - kt0):
-  // wait until this wave's DMA of stage kt landed, barrier, DMA of stage kt + 2 into the
-  // slot of stage kt - 1, B of step 2 kt + 1, step 2 kt, B of step 2 kt + 2, step 2 kt + 1
-  // (B is loaded one 64-deep step ahead). Loads issued after the DMA of stage kt: from
-  // the prologue PW + 2 FN (r = 0) and PW + 6 FN (r = 1); in steady state (r >= 2) the
-  // 4 FN B loads of the stage that issued it and one whole stage, PW + 8 FN.
+  // B is loaded two 64-deep steps ahead into two register sets. Stage kt (r = kt - kt0):
+  // wait until this wave's DMA of stage kt landed, barrier; step 2 kt, then B of step
+  // 2 kt + 2 into its set; step 2 kt + 1, then B of step 2 kt + 3; last, the DMA of stage
+  // kt + 2 into the slot of stage kt - 1. The compiler waits for a B set counting only the
+  // B loads issued after it, so each of its waits also retires the oldest DMA issued
+  // after that B load: with this order that is at most the DMA of stage kt + 1, in the
+  // second half of stage kt, just before it is needed (with FN = 1 the first wait of a
+  // stage retires half of it). Loads issued after the DMA of stage kt: PW + 4 FN
+  // (r = 0: the prologue's second DMA and B sets; steady state: stage kt - 1's B loads
+  // and DMA), 8 FN + PW (r = 1: the prologue's B sets and stage kt0's loads).
   static_assert(S == 3, "three LDS stages");
-  constexpr int W0 = PW + 2 * FN;
-  constexpr int W1 = PW + 6 * FN;
-  constexpr int WS = PW + 8 * FN;
-  static_assert(WS < 64, "vmcnt range");
+  constexpr int WS = PW + 4 * FN;
+  constexpr int W1 = 8 * FN + PW;
+  static_assert(W1 < 64, "vmcnt range");
   issue_a(kt0, 0);
   issue_a(kt0 + 1, 1);
   BStep b0, b1;
   load_b(2 * kt0, b0);
+  load_b(2 * kt0 + 1, b1);
   for (int kt = kt0; kt < kt1; ++kt) {
     const int r = kt - kt0;
-    if (r == 0)
-      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(W0));
-    else if (r == 1)
+    if (r == 1)
       __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(W1));
     else
       __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(WS));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    issue_a(kt + 2, (r + 2) % 3);
     const int slot = r % 3;
     v8i a[FM];
-    load_b(2 * kt + 1, b1);
     read_a(slot, 0, a);
     mfmas(a, b0);
     KSched<0, NM, 0, 0>::apply();
@@ -894,6 +911,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
     mfmas(a, b1);
     KSched<0, NM, 0, 0>::apply();
     __builtin_amdgcn_sched_barrier(0);
+    load_b(2 * kt + 3, b1);
+    issue_a(kt + 2, (r + 2) % 3);
   }
   __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
   __syncthreads();
