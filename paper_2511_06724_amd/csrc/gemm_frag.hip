@@ -13,7 +13,9 @@
 //    issue the loads);
 //  - block tile BM x NW * 32 FN: the NW (4 or 5) waves split the columns, each computes
 //    BM x 32 FN with 32x32x16 MFMAs issued as C^T = B A^T (four consecutive output
-//    columns per lane);
+//    columns per lane). The 160-column tiles take four waves (X5): wave w owns column
+//    block w and computes column block 4 over k-step w of every stage, so the four SIMDs
+//    carry equal work; the four partial sums of block 4 meet in LDS in wave order;
 //  - every k-step interleaves one MFMA, one LDS fragment read for the next k-step and
 //    its share of B loads (scheduling groups); the stage hand-over (wait + barrier)
 //    sits before the last k-step, whose MFMAs cover the first reads of the next stage;
@@ -134,10 +136,12 @@ __device__ __forceinline__ void store8(const GemmParams& p, int m, int n, const 
   }
 }
 
-template <int BM, int FN, int S, int NW> constexpr size_t frag_lds_bytes() {
+template <int BM, int FN, int S, int NW, bool X5 = false> constexpr size_t frag_lds_bytes() {
   constexpr size_t stages = size_t(S) * BM * kRowBytes;
   constexpr size_t epi = size_t(NW) * 32 * (32 * FN + 4) * 4;
-  return stages > epi ? stages : epi;
+  constexpr size_t part5 = X5 ? size_t(4) * (BM / 32) * 16 * 64 * 4 : 0;  // block-4 partial sums
+  constexpr size_t m1 = stages > epi ? stages : epi;
+  return m1 > part5 ? m1 : part5;
 }
 
 // MODE: 0 linear layer (one A source), 1 linear layer over two concatenated A sources,
@@ -147,13 +151,16 @@ template <int BM, int FN, int S, int NW> constexpr size_t frag_lds_bytes() {
 // epilogue overlap the other's MFMAs). PRE: read a whole LDS stage of A fragments one
 // stage ahead into registers (small tiles, whose few MFMAs per k-step cannot cover an
 // LDS read latency), instead of one k-step ahead. NW: waves per workgroup, each owning
-// 32 FN columns; with five (a 160-column tile) the first four issue the A DMA.
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW = 4>
+// 32 FN columns; with five (a 160-column tile) the first four issue the A DMA. X5: the
+// 160-column tile on four waves (see the file comment).
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW = 4, bool X5 = false>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_frag_kernel(
     GemmParams p, int mt, int nt, int nsplit) {
   constexpr int FM = BM / 32;
   constexpr int WN = 32 * FN;
-  constexpr int BN = NW * WN;
+  constexpr int BN = X5 ? 160 : NW * WN;
+  static_assert(!X5 || (NW == 4 && FN == 1 && !PRE), "X5: four waves of one column block each");
+  constexpr int NB = 4 * FN + (X5 ? 1 : 0);  // B loads per wave and stage
   constexpr int STAGE = BM * kRowBytes;
   constexpr int PW = BM / 32;  // DMA instructions (8 rows of 128 B) per DMA wave per stage
   static_assert(NW == 4 || NW == 5, "four or five waves");
@@ -282,6 +289,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
 #pragma unroll
     for (int j = 0; j < FN; ++j) dst[s][j] = *reinterpret_cast<const bf16x8*>(bptr[j] + (kt * 4 + s) * 512);
   };
+  // X5: the fragment of column block 4 for k-step `wave` of a stage
+  const bf16* const bptr5 =
+      static_cast<const bf16*>(p.b) + (long long)min(n0 / 32 + 4, nb_last) * kbs * 512 + lane * 8 + wave * 512;
+  auto load_b5 = [&](int kt_in, bf16x8& dst) {
+    const int kt = kt_in < kt1 ? kt_in : kt1 - 1;
+    dst = *reinterpret_cast<const bf16x8*>(bptr5 + kt * 4 * 512);
+  };
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -290,6 +304,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
     for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  f32x16 acc5[X5 ? FM : 1];
+#pragma unroll
+  for (int i = 0; i < (X5 ? FM : 1); ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc5[i][r] = 0.f;
 
   // Epilogue input of the plain path (the residual or the per-sample row vector, when
   // exactly one is present) for small wave tiles of the linear modes without stage
@@ -348,6 +367,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
       for (int j = 0; j < FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
   };
+  bf16x8 a5[X5 ? FM : 1];
+  auto mfmas5 = [&](const bf16x8& b) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) acc5[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a5[i], acc5[i], 0, 0, 0);
+  };
 
   BReg bq[D];
   if constexpr (PRE) {
@@ -405,18 +429,30 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
     if (kt < kt1) pstage(kt, sa[0], sa[1], bq[0]);
   } else {
     BReg bq[D];
+    bf16x8 b5q[X5 ? D : 1];
     // One k-step: [the DMA of a later A stage first, when `dma`], the next k-step's A
     // fragments from LDS, this k-step's MFMAs and the B loads of stage kt + D for this
-    // k-step, interleaved one MFMA / one LDS read / a share of the VM loads.
-    auto kstep = [&](auto dma, int dma_kt, int dma_slot, int rd_slot, int rd_s, bf16x8* a_use, bf16x8* a_next,
-                     bf16x8* b_use, int bkt, int s, BReg& bb) {
+    // k-step, interleaved one MFMA / one LDS read / a share of the VM loads. X5 (part):
+    // k-step 0 also reads the A fragments of k-step `wave` of the stage, k-step 1 runs
+    // the column-block-4 MFMAs on them, k-step 2 loads the block-4 fragment of stage
+    // kt + D (after its use).
+    auto kstep = [&](auto dma, auto part, int dma_kt, int dma_slot, int rd_slot, int rd_s, bf16x8* a_use,
+                     bf16x8* a_next, bf16x8* b_use, int bkt, int s, BReg& bb, bf16x8& b5) {
+      constexpr int X = X5 ? decltype(part)::value : 0;
       if constexpr (decltype(dma)::value) issue_a(dma_kt, dma_slot);
       read_a(rd_slot, rd_s, a_next);
+      if constexpr (X == 1) read_a(rd_slot, wave, a5);
       mfmas(a_use, b_use);
+      if constexpr (X == 2) mfmas5(b5);
       load_b_step(bkt, s, bb);
-      KSched<0, NM, FM, FN>::apply();
+      if constexpr (X == 3) load_b5(bkt, b5);
+      KSched<0, NM + (X == 2 ? FM : 0), FM, FN + (X == 3 ? 1 : 0)>::apply();
       __builtin_amdgcn_sched_barrier(0);
     };
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    using P2 = std::integral_constant<int, 2>;
+    using P3 = std::integral_constant<int, 3>;
 
     // prologue: A stages kt0 .. kt0 + S - 1 (every slot), B stages kt0 .. kt0 + D - 1; the
     // wait covers A stages kt0 .. kt0 + Q (see the hand-over below)
@@ -424,14 +460,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   #pragma unroll
     for (int s = 0; s < S; ++s) issue_a(kt0 + s, s);
   #pragma unroll
-    for (int d = 0; d < D; ++d)
+    for (int d = 0; d < D; ++d) {
   #pragma unroll
       for (int s = 0; s < 4; ++s) load_b_step(kt0 + d, s, bq[d]);
+      if constexpr (X5) load_b5(kt0 + d, b5q[d]);
+    }
     // the epilogue inputs come after every prologue load: the waits below count only
     // loads issued after their target, so more of them (these) keep the waits exact or
     // conservative
     load_pre_in();
-    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((S - 1 - Q) * PW + D * 4 * FN));
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((S - 1 - Q) * PW + D * NB));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     read_a(0, 0, fa[0]);
@@ -441,46 +479,47 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
     // after the barrier every wave's has, and every wave is done reading slot kt; then
     // k-step 3 issues stage kt + S into that slot and reads stage kt + 1's first fragments.
     // VM loads issued after the DMA of stage kt + 1 (made in k-step 3 of stage kt + 1 - S):
-    // B(3) of that stage, S - 2 whole stages (4 FN B loads + PW DMA each), B(0..2) of stage kt.
-    // When stage kt + 1 (kt = kt0 + r) came from the prologue, the loads after its DMA are
-    // (S - 2 - r) PW + 4 D FN + r (4 FN + PW) + 3 FN, at least VM_END once D + r >= S - 1;
-    // the prologue itself waited for stages up to kt0 + Q, Q = max(1, S - 1 - D).
-    constexpr int VM_END = 4 * FN + (S - 2) * (4 * FN + PW);
-    static_assert(VM_END < 64 && (S - 1 - Q) * PW + D * 4 * FN < 64, "vmcnt range");
-    auto stage = [&](int kt, BReg& bb) {
+    // B(3) of that stage, S - 2 whole stages (NB B loads + PW DMA each), the B loads of
+    // k-steps 0..2 of stage kt (NB - FN). When stage kt + 1 (kt = kt0 + r) came from the
+    // prologue, the loads after its DMA are (S - 2 - r) PW + D NB + r (NB + PW) + NB - FN,
+    // at least VM_END once D + r >= S - 1; the prologue itself waited for stages up to
+    // kt0 + Q, Q = max(1, S - 1 - D).
+    constexpr int VM_END = NB + (S - 2) * (NB + PW);
+    static_assert(VM_END < 64 && (S - 1 - Q) * PW + D * NB < 64, "vmcnt range");
+    auto stage = [&](int kt, BReg& bb, bf16x8& b5) {
       const int rel = kt - kt0;
       const int slot = rel % S;
       const int nslot = (rel + 1) % S;
-      kstep(std::false_type{}, 0, 0, slot, 1, fa[0], fa[1], bb[0], kt + D, 0, bb);
-      kstep(std::false_type{}, 0, 0, slot, 2, fa[1], fa[0], bb[1], kt + D, 1, bb);
-      kstep(std::false_type{}, 0, 0, slot, 3, fa[0], fa[1], bb[2], kt + D, 2, bb);
+      kstep(std::false_type{}, P1{}, 0, 0, slot, 1, fa[0], fa[1], bb[0], kt + D, 0, bb, b5);
+      kstep(std::false_type{}, P2{}, 0, 0, slot, 2, fa[1], fa[0], bb[1], kt + D, 1, bb, b5);
+      kstep(std::false_type{}, P3{}, 0, 0, slot, 3, fa[0], fa[1], bb[2], kt + D, 2, bb, b5);
       __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(VM_END));
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      kstep(std::true_type{}, kt + S, slot, nslot, 0, fa[1], fa[0], bb[3], kt + D, 3, bb);
+      kstep(std::true_type{}, P0{}, kt + S, slot, nslot, 0, fa[1], fa[0], bb[3], kt + D, 3, bb, b5);
     };
 
     if constexpr (D == 3) {
       // Triples of stages, then the rest (as for pairs below)
       int kt = kt0;
       for (; kt + 2 < kt1; kt += 3) {
-        stage(kt, bq[0]);
-        stage(kt + 1, bq[1]);
-        stage(kt + 2, bq[2]);
+        stage(kt, bq[0], b5q[0]);
+        stage(kt + 1, bq[1], b5q[X5 ? 1 : 0]);
+        stage(kt + 2, bq[2], b5q[X5 ? 2 : 0]);
       }
-      if (kt < kt1) stage(kt, bq[0]);
-      if (kt + 1 < kt1) stage(kt + 1, bq[1]);
+      if (kt < kt1) stage(kt, bq[0], b5q[0]);
+      if (kt + 1 < kt1) stage(kt + 1, bq[1], b5q[X5 ? 1 : 0]);
     } else if constexpr (D == 2) {
       // Pairs of stages, then the odd one: no stage of the loop body is conditional, so
       // the compiler's wait for a B register counts both stages' loads issued after it.
       int kt = kt0;
       for (; kt + 1 < kt1; kt += 2) {
-        stage(kt, bq[0]);
-        stage(kt + 1, bq[1]);
+        stage(kt, bq[0], b5q[0]);
+        stage(kt + 1, bq[1], b5q[X5 ? 1 : 0]);
       }
-      if (kt < kt1) stage(kt, bq[0]);
+      if (kt < kt1) stage(kt, bq[0], b5q[0]);
     } else {
-      for (int kt = kt0; kt < kt1; ++kt) stage(kt, bq[0]);
+      for (int kt = kt0; kt < kt1; ++kt) stage(kt, bq[0], b5q[0]);
     }
   }
   // The loads past the range (zero block, clamped B) must land before LDS is reused.
@@ -491,7 +530,27 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   const int col = lane & 31;
   const int h4 = 4 * (lane >> 5);
   const int nw0 = n0 + wave * WN;
-  if (!SPLIT && p.vt && nw0 + WN > p.vt_col0) {
+  // X5: the partial sums of column block 4 go to LDS in the register layout; wave w < FM
+  // then sums row block w of it over the four waves in wave order.
+  f32x16 acc5t;
+  if constexpr (X5) {
+    float* part5 = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) part5[((wave * FM + i) * 16 + r) * 64 + lane] = acc5[i][r];
+    __syncthreads();
+    if (wave < FM) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc5t[r] = part5[((0 * FM + wave) * 16 + r) * 64 + lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc5t[r] += part5[((w * FM + wave) * 16 + r) * 64 + lane];
+    }
+    __syncthreads();
+  }
+  if (!X5 && !SPLIT && p.vt && nw0 + WN > p.vt_col0) {
     // columns of the per-head V^T output (or a wave straddling it): register layout,
     // lanes 0..31 = 32 consecutive tokens of one column
 #pragma unroll
@@ -514,15 +573,18 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   constexpr int EPL = WN + 4;
   float* ep = reinterpret_cast<float*>(smem) + wave * (32 * EPL);
   float* slab = SPLIT ? p.part + (long long)split * p.M * p.n_store : nullptr;
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
+  // One 32-row block of this wave's columns [nw0, nw0 + WN): blk[j] the accumulators of
+  // column block j, rows mb .. mb + 31; i < 0: no preloaded epilogue input (the extra
+  // column-block-4 block of X5), else its row block.
+  auto epi_block = [&](const f32x16* blk, const int mb, const int nw0, const int i) {
+    const bool pre_in_b = pre_in && i >= 0;
+    const int ip = i >= 0 ? i : 0;
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
         *reinterpret_cast<f32x4*>(ep + col * EPL + j * 32 + 8 * g + h4) =
-            f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-    const int mb = m0 + i * 32;
+            f32x4{blk[j][4 * g], blk[j][4 * g + 1], blk[j][4 * g + 2], blk[j][4 * g + 3]};
     if (SPLIT) {
       constexpr int LPR = WN / 4;   // lanes per row
       constexpr int RPI = 64 / LPR; // rows per pass
@@ -555,7 +617,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
         const int m = mb + t * RPI + lane / LPR;
 #pragma unroll
         for (int e = 0; e < 8; ++e) rv[t][e] = rs[t][e] = 0.f;
-        if (m >= p.M || !ncol || pre_in) continue;
+        if (m >= p.M || !ncol || pre_in_b) continue;
         if (p.rowvec) load_rowvec8(p, m, n, rv[t]);
         if (p.resid) load_resid8(p, m, n, rvec, rs[t]);
       }
@@ -576,9 +638,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
           float x = e < 4 ? a0[e] : a1[e - 4];
           if (p.bias) x += bias8[e];
           if constexpr (kPreIn) {
-            if (pre_in) x += pin[i][t][e / 4][e % 4];
+            if (pre_in_b) x += pin[ip][t][e / 4][e % 4];
           }
-          if (!pre_in) {
+          if (!pre_in_b) {
             if (p.rowvec) x += rv[t][e];
             if (p.resid) x += rs[t][e];
           }
@@ -639,6 +701,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
         }
       }
     }
+  };
+#pragma unroll
+  for (int i = 0; i < FM; ++i) epi_block(acc[i], m0 + i * 32, nw0, i);
+  if constexpr (X5) {
+    if (wave < FM) epi_block(&acc5t, m0 + wave * 32, n0 + 128, -1);
   }
 }
 
@@ -683,37 +750,40 @@ void splitk_reduce(const GemmParams& p, int nsplit, hipStream_t s) {
   DN_HIP(hipGetLastError());
 }
 
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW>
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW, bool X5>
 void launch_frag(const GemmParams& p, int nsplit, hipStream_t s) {
-  constexpr size_t lds = frag_lds_bytes<BM, FN, S, NW>();
+  constexpr size_t lds = frag_lds_bytes<BM, FN, S, NW, X5>();
   static bool attr_set = false;
   if (!attr_set) {
-    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW>),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+    DN_HIP(hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
     attr_set = true;
   }
-  const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, 32 * FN * NW);
-  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW>), dim3(mt * nt * nsplit), dim3(64 * NW),
-                     lds, s, p, mt, nt, nsplit);
+  const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, X5 ? 160 : 32 * FN * NW);
+  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5>), dim3(mt * nt * nsplit),
+                     dim3(64 * NW), lds, s, p, mt, nt, nsplit);
   DN_HIP(hipGetLastError());
 }
 
-template <int BM, int FN, int S, int D, int WPE, int MODE, int PRE = 0, int NW = 4>
+template <int BM, int FN, int S, int D, int WPE, int MODE, int PRE = 0, int NW = 4, bool X5 = false>
 void run_frag(const GemmParams& p, int nsplit, hipStream_t s) {
   if (p.raw_partial) {
-    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE, NW>(p, nsplit, s);
+    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE, NW, X5>(p, nsplit, s);
   } else if (nsplit > 1) {
-    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE, NW>(p, nsplit, s);
+    launch_frag<BM, FN, S, D, WPE, MODE, true, PRE, NW, X5>(p, nsplit, s);
     splitk_reduce(p, nsplit, s);
   } else {
-    launch_frag<BM, FN, S, D, WPE, MODE, false, PRE, NW>(p, 1, s);
+    launch_frag<BM, FN, S, D, WPE, MODE, false, PRE, NW, X5>(p, 1, s);
   }
 }
 
-// Tile plans (three LDS stages): 128 x 256 (FN = 2) with one B buffer, two workgroups per
-// CU; 128 x 128 (FN = 1) and 64 x 128 with two B buffers, two / four workgroups per CU;
-// 64 x 160 and 128 x 160 (five waves) with two B buffers, one workgroup per CU.
-// stages = 2 selects the 128 x 256 variant with two B buffers and one workgroup per CU.
+// Tile plans (three LDS stages): 128 x 256 (FN = 2) with two B buffers (one for the
+// convolution), two workgroups per CU; 128 x 128 (FN = 1) and 64 x 128 with two B buffers,
+// two / four workgroups per CU; 64 x 160 and 128 x 160 on five waves with three B buffers,
+// one workgroup per CU, or (stages = 5) on four waves (X5) with three / two B buffers, two
+// workgroups per CU. stages = 2 selects the 128 x 256 variant with two B buffers and one
+// workgroup per CU.
 template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
   if (g.bm == 128 && g.bn == 256 && g.stages == 3) {
     // B two stages ahead where the registers allow it (the implicit convolution's
@@ -732,9 +802,11 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   if (g.bm == 64 && g.bn == 256 && g.stages == 13) return run_frag<64, 2, 3, 2, 2, MODE, 1>(p, g.split, s);
   if (g.bm == 32 && g.bn == 128 && g.stages == 13) return run_frag<32, 1, 3, 2, 4, MODE, 1>(p, g.split, s);
   if constexpr (MODE != 2) {
-    if (g.bm == 64 && g.bn == 160 && g.stages == 3) return run_frag<64, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
+    if (g.bm == 64 && g.bn == 160 && (g.stages == 3 || p.vt)) return run_frag<64, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
+    if (g.bm == 64 && g.bn == 160 && g.stages == 5) return run_frag<64, 1, 3, 3, 2, MODE, 0, 4, true>(p, g.split, s);
   }
-  if (g.bm == 128 && g.bn == 160 && g.stages == 3) return run_frag<128, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
+  if (g.bm == 128 && g.bn == 160 && (g.stages == 3 || p.vt)) return run_frag<128, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
+  if (g.bm == 128 && g.bn == 160 && g.stages == 5) return run_frag<128, 1, 3, 2, 2, MODE, 0, 4, true>(p, g.split, s);
   throw Error(-1, "gemm: no fragment-B kernel for this tile plan");
 }
 

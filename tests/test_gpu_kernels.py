@@ -96,8 +96,14 @@ def test_linear_geglu(dtype, M, N, K):
 
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("n,H,W,Cin,Cout,up,stride", [
-    (2, 9, 7, 64, 96, 0, 1), (2, 9, 7, 64, 96, 0, 2), (1, 5, 6, 128, 64, 1, 1), (2, 16, 16, 128, 320, 0, 1)])
+    (2, 9, 7, 64, 96, 0, 1), (2, 9, 7, 64, 96, 0, 2), (1, 5, 6, 128, 64, 1, 1), (2, 16, 16, 128, 320, 0, 1),
+    (2, 128, 128, 320, 320, 0, 1), (2, 128, 128, 640, 320, 0, 1), (1, 64, 64, 640, 640, 1, 1)])
 def test_conv3x3(dtype, n, H, W, Cin, Cout, up, stride):
+    """Small shapes with ragged tiles, and the SD-XL convolutions at full size, whole
+    output against the oracle: the 128x128-level ResBlock convolutions (32768 rows, 320
+    channels from 320 and from a 640-channel input) and the nearest-x2 upsampling
+    convolution into that level (640 channels): in bf16 these run on the four-wave
+    160-column tiles, two workgroups per CU."""
     announce(f"conv dtype={dtype} n={n} H={H} W={W} Cin={Cin} Cout={Cout} up={up} stride={stride}")
     r = _rng(n * H * W + Cin + Cout + up + stride)
     x, xh = to_dev(r.standard_normal((n, H, W, Cin)), dtype)
