@@ -324,12 +324,25 @@ GemmPlan frag_plan(int M, int N, int K, int geglu, int cus, bool allow_split, bo
       }
     }
   }
-  // 128 x 160 tiles that fill more than one workgroup per CU run on four waves, two
-  // workgroups per CU (the five-wave tile leaves one SIMD with two waves' work and one
-  // workgroup per CU): measured 17 % faster for the 32768-row convolutions; with one
-  // tile per CU the five-wave tile is as fast or faster
-  if (best.bm == 128 && best.bn == 160 && (long long)ceil_div(M, 128) * ceil_div(N, 160) * best.split > cus)
+  // 128 x 160 tiles run on four waves, two workgroups per CU (the five-wave tile leaves
+  // one SIMD with two waves' work and one workgroup per CU) for every convolution
+  // (measured: 32768-row convolutions 17 % faster, the 8192-row upsampling convolution
+  // from 1280 channels 373 -> 268 us, the other 8192-row ones equal or up to 6 % faster)
+  // and for linear layers with more tiles than CUs; with one tile per CU the linear
+  // layers run as fast or faster on five waves
+  if (best.bm == 128 && best.bn == 160 &&
+      (conv || (long long)ceil_div(M, 128) * ceil_div(N, 160) * best.split > cus))
     best.stages = 5;
+  // 128 x 256 linear tiles (two workgroups per CU) whose count leaves a last round at most
+  // half full: those last whole column bands run as 64-row tiles over every CU
+  if (!conv && best.bm == 128 && best.bn == 256 && best.split == 1) {
+    const long long mt = ceil_div(M, 128), nt = ceil_div(N, 256), slots = 2LL * cus;
+    const long long tiles = mt * nt, rem = tiles % slots;
+    if (rem > 0 && 2 * rem <= slots && rem % mt == 0) {
+      const long long bands = rem / mt, tail = (long long)ceil_div(M, 64) * bands;
+      if ((tiles - rem) % 8 == 0 && tail % 8 == 0 && bands < nt) best.tail_bands = static_cast<int>(bands);
+    }
+  }
   return best;
 }
 

@@ -153,9 +153,11 @@ template <int BM, int FN, int S, int NW, bool X5 = false> constexpr size_t frag_
 // LDS read latency), instead of one k-step ahead. NW: waves per workgroup, each owning
 // 32 FN columns; with five (a 160-column tile) the first four issue the A DMA. X5: the
 // 160-column tile on four waves (see the file comment).
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW = 4, bool X5 = false>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_frag_kernel(
-    GemmParams p, int mt, int nt, int nsplit) {
+// One unit: the BM x BN tile at (m0, n0) over the K stages [kt0, kt1) (split-K part
+// `split` when SPLIT).
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW, bool X5>
+__device__ __forceinline__ void frag_tile(const GemmParams& p, const int m0, const int n0, const int split,
+                                          const int kt0, const int kt1) {
   constexpr int FM = BM / 32;
   constexpr int WN = 32 * FN;
   constexpr int BN = X5 ? 160 : NW * WN;
@@ -170,21 +172,6 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   static_assert(BM % 32 == 0 && BM <= 256, "BM");
 
   extern __shared__ __align__(16) unsigned char smem[];
-
-  // ---- unit assignment (see the file comment)
-  const int units = mt * nt * nsplit;
-  const int wg = blockIdx.x;
-  const int xcd = wg % kXcds, idx = wg / kXcds;
-  const int base = units / kXcds, rem = units % kXcds;
-  const int logical = xcd * base + min(xcd, rem) + idx;
-  const int m_tile = logical % mt;
-  const int ns = logical / mt;
-  const int split = ns % nsplit;
-  const int n_tile = ns / nsplit;
-  const int n0 = n_tile * BN, m0 = m_tile * BM;
-  const int nk = p.K / kBK;
-  const int kt0 = (int)((long long)split * nk / nsplit);
-  const int kt1 = (int)((long long)(split + 1) * nk / nsplit);
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -709,6 +696,50 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WP
   }
 }
 
+// The kernel: unit assignment (see the file comment), then the unit's tile. TBM > 0 with
+// tail_bands > 0 (no split): the first tail_full units are BM-row tiles of the column
+// bands before the last tail_bands, the rest TBM-row tiles of those last bands; each
+// XCD takes its share of both kinds, full tiles first (tail_full and the tail count
+// are multiples of the XCD count). A grid of BM-row tiles that fills a whole number of
+// rounds plus a fraction of one leaves that fraction to half the CUs; TBM-row tiles
+// spread it over all of them.
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW = 4, bool X5 = false,
+          int TBM = 0>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_frag_kernel(
+    GemmParams p, int mt, int nt, int nsplit, int tail_full, int tail_bands) {
+  constexpr int BN = X5 ? 160 : NW * 32 * FN;
+  const int wg = blockIdx.x;
+  const int xcd = wg % kXcds, idx = wg / kXcds;
+  const int nk = p.K / kBK;
+  if constexpr (TBM > 0) {
+    static_assert(!SPLIT, "tail tiles take no split");
+    if (tail_bands > 0) {
+      const int fx = tail_full / kXcds;
+      const int tm = (p.M + TBM - 1) / TBM;
+      const int tx = tm * tail_bands / kXcds;
+      if (idx < fx) {
+        const int f = xcd * fx + idx;
+        frag_tile<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5>(p, (f % mt) * BM, (f / mt) * BN, 0, 0, nk);
+      } else {
+        const int t = xcd * tx + (idx - fx);
+        frag_tile<TBM, FN, S, 1, WPE, MODE, SPLIT, PRE, NW, X5>(p, (t % tm) * TBM,
+                                                                (nt - tail_bands + t / tm) * BN, 0, 0, nk);
+      }
+      return;
+    }
+  }
+  const int units = mt * nt * nsplit;
+  const int base = units / kXcds, rem = units % kXcds;
+  const int logical = xcd * base + min(xcd, rem) + idx;
+  const int m_tile = logical % mt;
+  const int ns = logical / mt;
+  const int split = ns % nsplit;
+  const int n_tile = ns / nsplit;
+  const int kt0 = (int)((long long)split * nk / nsplit);
+  const int kt1 = (int)((long long)(split + 1) * nk / nsplit);
+  frag_tile<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5>(p, m_tile * BM, n_tile * BN, split, kt0, kt1);
+}
+
 // Sum of the split-K partial slabs [NS][M][n_store] in split order, then the epilogue;
 // one thread per 4 consecutive columns of a row, all slab loads issued before the sum.
 template <int NS> __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p) {
@@ -750,19 +781,29 @@ void splitk_reduce(const GemmParams& p, int nsplit, hipStream_t s) {
   DN_HIP(hipGetLastError());
 }
 
-template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW, bool X5>
-void launch_frag(const GemmParams& p, int nsplit, hipStream_t s) {
-  constexpr size_t lds = frag_lds_bytes<BM, FN, S, NW, X5>();
+template <int BM, int FN, int S, int D, int WPE, int MODE, bool SPLIT, int PRE, int NW, bool X5, int TBM = 0>
+void launch_frag(const GemmParams& p, int nsplit, hipStream_t s, int tail_bands = 0) {
+  constexpr size_t lds_full = frag_lds_bytes<BM, FN, S, NW, X5>();
+  constexpr size_t lds_tail = TBM > 0 ? frag_lds_bytes<(TBM > 0 ? TBM : BM), FN, S, NW, X5>() : 0;
+  constexpr size_t lds = lds_full > lds_tail ? lds_full : lds_tail;
   static bool attr_set = false;
   if (!attr_set) {
     DN_HIP(hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5>),
+        reinterpret_cast<const void*>(&gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5, TBM>),
         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
     attr_set = true;
   }
   const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, X5 ? 160 : 32 * FN * NW);
-  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5>), dim3(mt * nt * nsplit),
-                     dim3(64 * NW), lds, s, p, mt, nt, nsplit);
+  int grid = mt * nt * nsplit, tail_full = 0;
+  if (TBM > 0 && tail_bands > 0) {
+    tail_full = mt * (nt - tail_bands);
+    const int tail = ceil_div(p.M, TBM > 0 ? TBM : BM) * tail_bands;
+    DN_CHECK(nsplit == 1 && tail_bands < nt && tail_full % kXcds == 0 && tail % kXcds == 0,
+             "gemm: tail tiles need no split and tile counts divisible by the XCD count");
+    grid = tail_full + tail;
+  }
+  hipLaunchKernelGGL((gemm_frag_kernel<BM, FN, S, D, WPE, MODE, SPLIT, PRE, NW, X5, TBM>), dim3(grid), dim3(64 * NW),
+                     lds, s, p, mt, nt, nsplit, tail_full, TBM > 0 ? tail_bands : 0);
   DN_HIP(hipGetLastError());
 }
 
@@ -788,10 +829,16 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   if (g.bm == 128 && g.bn == 256 && g.stages == 3) {
     // B two stages ahead where the registers allow it (the implicit convolution's
     // address registers do not leave room)
-    if constexpr (MODE == 2)
+    if constexpr (MODE == 2) {
       return run_frag<128, 2, 3, 1, 2, MODE>(p, g.split, s);
-    else
+    } else {
+      // the last column bands of a grid with a partial last round as 64-row tiles
+      if (g.tail_bands > 0 && g.split == 1 && !p.raw_partial) {
+        launch_frag<128, 2, 3, 2, 2, MODE, false, 0, 4, false, 64>(p, 1, s, g.tail_bands);
+        return;
+      }
       return run_frag<128, 2, 3, 2, 2, MODE>(p, g.split, s);
+    }
   }
   if (g.bm == 128 && g.bn == 256 && g.stages == 2) return run_frag<128, 2, 3, 2, 1, MODE>(p, g.split, s);
   if (g.bm == 128 && g.bn == 128 && g.stages == 3) return run_frag<128, 1, 3, 2, 2, MODE>(p, g.split, s);
@@ -803,7 +850,10 @@ template <int MODE> void dispatch_frag(const GemmParams& p, const GemmPlan& g, h
   if (g.bm == 32 && g.bn == 128 && g.stages == 13) return run_frag<32, 1, 3, 2, 4, MODE, 1>(p, g.split, s);
   if constexpr (MODE != 2) {
     if (g.bm == 64 && g.bn == 160 && (g.stages == 3 || p.vt)) return run_frag<64, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
+  }
+  if (!p.vt) {
     if (g.bm == 64 && g.bn == 160 && g.stages == 5) return run_frag<64, 1, 3, 3, 2, MODE, 0, 4, true>(p, g.split, s);
+    if (g.bm == 32 && g.bn == 160 && g.stages == 5) return run_frag<32, 1, 3, 3, 2, MODE, 0, 4, true>(p, g.split, s);
   }
   if (g.bm == 128 && g.bn == 160 && (g.stages == 3 || p.vt)) return run_frag<128, 1, 3, 3, 2, MODE, 0, 5>(p, g.split, s);
   if (g.bm == 128 && g.bn == 160 && g.stages == 5) return run_frag<128, 1, 3, 2, 2, MODE, 0, 4, true>(p, g.split, s);
@@ -1185,6 +1235,7 @@ GemmPlan gemm_plan_fp8(int M, int N, int K, int geglu, int cus, bool allow_split
   while (g.split > 1 && K / 128 < 2 * g.split) --g.split;
   g.frag = 1;
   g.stages = 3;
+  g.tail_bands = 0;
   return g;
 }
 

@@ -61,6 +61,7 @@ struct GemmPlan {
   int stages = 2;        // fragment-B kernel: LDS pipeline depth
   int frag = 0;          // 1: bf16 fragment-B kernel (gemm_frag.hip), else the register-staged kernel
   int split = 1;         // fragment-B kernel: K split in this many ranges (fp32 partials + reduce)
+  int tail_bands = 0;    // fragment-B 128 x 256 tiles: the last column bands as 64-row tiles
 };
 constexpr int kMaxSplit = 8;
 // allow_split = false for epilogues split-K does not support (the per-head V^T output);

@@ -76,8 +76,10 @@ def _interleave(w1, n):
 
 
 @pytest.mark.parametrize("dtype", DT)
-@pytest.mark.parametrize("M,N,K", [(300, 96, 128), (512, 1280, 320)])
+@pytest.mark.parametrize("M,N,K", [(300, 96, 128), (512, 1280, 320), (2048, 5120, 1280)])
 def test_linear_geglu(dtype, M, N, K):
+    """Ragged small shapes and SD-XL's FF-in at full size, whole output: in bf16 its 640
+    128 x 256 tiles leave a quarter round, whose column bands run as 64-row tiles."""
     announce(f"geglu dtype={dtype} M={M} N={N} K={K}")
     r = _rng(7 * M + N)
     x, xh = to_dev(r.standard_normal((M, K)), dtype)
