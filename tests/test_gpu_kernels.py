@@ -36,14 +36,16 @@ def _rng(seed):
 @pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280),
                                    (2048, 2048, 128), (8192, 512, 256), (300, 1280, 2560), (77, 96, 1920),
                                    (1000, 640, 5120), (129, 256, 704), (2000, 1248, 1280), (8000, 608, 2560),
-                                   (8192, 200, 256)])
+                                   (8192, 200, 256), (16384, 640, 1280), (2048, 10240, 1280)])
 def test_linear(dtype, M, N, K):
     """Shapes cover every tile plan: in fp32 the register-staged 64 x 64 / 128 x 128
     tiles; in bf16 the row-major kernels for N % 32 != 0 (N = 200) and the fragment-B
     kernel with 128 x 128 and 128 x 256 tiles, with and without split-K (few tiles and
     long K: 300 x 1280 x 2560, 1000 x 640 x 5120), the five-wave 64 x 160 and 128 x 160
     tiles (2000 x 1248 x 1280, 8000 x 608 x 2560: one tile per CU, ragged last row tile
-    and column tile), ragged M and N tails; a tall row-major case (8192 x 200 x 256). Outputs: bf16 / fp32 without residual, fp32
+    and column tile), ragged M and N tails; a tall row-major case (8192 x 200 x 256); the
+    four-wave 128 x 160 tiles, two per CU, that linear layers with more 160-column tiles
+    than CUs take (16384 x 640 x 1280, 2048 x 10240 x 1280). Outputs: bf16 / fp32 without residual, fp32
     with an fp32 residual, and the op's dtype with a residual in that dtype."""
     announce(f"linear dtype={dtype} M={M} N={N} K={K}")
     r = _rng(M + N + K)
