@@ -893,8 +893,8 @@ __device__ __forceinline__ void store8_fp8(const GemmParams& p, int m, int n, co
 }
 
 template <int BM, int FN, int S, int WPE, bool SPLIT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_fp8_kernel(
-    GemmParams p, int mt, int nt, int nsplit) {
+__device__ __forceinline__ void fp8_tile(const GemmParams& p, const int m0, const int n0, const int split,
+                                         const int kt0, const int kt1) {
   constexpr int NW = 4;
   constexpr int FM = BM / 32;
   constexpr int WN = 32 * FN;
@@ -905,20 +905,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
   static_assert(S >= 3 && S <= 4, "three or four LDS stages");
 
   extern __shared__ __align__(16) unsigned char smem[];
-
-  const int units = mt * nt * nsplit;
-  const int wg = blockIdx.x;
-  const int xcd = wg % kXcds, idx = wg / kXcds;
-  const int base = units / kXcds, rem = units % kXcds;
-  const int logical = xcd * base + min(xcd, rem) + idx;
-  const int m_tile = logical % mt;
-  const int ns = logical / mt;
-  const int split = ns % nsplit;
-  const int n_tile = ns / nsplit;
-  const int n0 = n_tile * BN, m0 = m_tile * BM;
-  const int nk = p.K / 128;
-  const int kt0 = (int)((long long)split * nk / nsplit);
-  const int kt1 = (int)((long long)(split + 1) * nk / nsplit);
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1158,18 +1144,65 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
   }
 }
 
-template <int BM, int FN, int S, int WPE, bool SPLIT>
-void launch_fp8(const GemmParams& p, int nsplit, hipStream_t s) {
-  constexpr size_t lds = frag_lds_bytes<BM, FN, S, 4>();
+// The fp8 kernel: unit assignment as gemm_frag_kernel (XCD-contiguous; with TBM > 0 and
+// tail_bands > 0 the last column bands as TBM-row tiles, full tiles first on every XCD).
+template <int BM, int FN, int S, int WPE, bool SPLIT, int TBM = 0>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void gemm_fp8_kernel(
+    GemmParams p, int mt, int nt, int nsplit, int tail_full, int tail_bands) {
+  constexpr int BN = 4 * 32 * FN;
+  const int wg = blockIdx.x;
+  const int xcd = wg % kXcds, idx = wg / kXcds;
+  const int nk = p.K / 128;
+  if constexpr (TBM > 0) {
+    static_assert(!SPLIT, "tail tiles take no split");
+    if (tail_bands > 0) {
+      const int fx = tail_full / kXcds;
+      const int tm = (p.M + TBM - 1) / TBM;
+      const int tx = tm * tail_bands / kXcds;
+      if (idx < fx) {
+        const int f = xcd * fx + idx;
+        fp8_tile<BM, FN, S, WPE, SPLIT>(p, (f % mt) * BM, (f / mt) * BN, 0, 0, nk);
+      } else {
+        const int t = xcd * tx + (idx - fx);
+        fp8_tile<TBM, FN, S, WPE, SPLIT>(p, (t % tm) * TBM, (nt - tail_bands + t / tm) * BN, 0, 0, nk);
+      }
+      return;
+    }
+  }
+  const int units = mt * nt * nsplit;
+  const int base = units / kXcds, rem = units % kXcds;
+  const int logical = xcd * base + min(xcd, rem) + idx;
+  const int m_tile = logical % mt;
+  const int ns = logical / mt;
+  const int split = ns % nsplit;
+  const int n_tile = ns / nsplit;
+  const int kt0 = (int)((long long)split * nk / nsplit);
+  const int kt1 = (int)((long long)(split + 1) * nk / nsplit);
+  fp8_tile<BM, FN, S, WPE, SPLIT>(p, m_tile * BM, n_tile * BN, split, kt0, kt1);
+}
+
+template <int BM, int FN, int S, int WPE, bool SPLIT, int TBM = 0>
+void launch_fp8(const GemmParams& p, int nsplit, hipStream_t s, int tail_bands = 0) {
+  constexpr size_t lds_full = frag_lds_bytes<BM, FN, S, 4>();
+  constexpr size_t lds_tail = TBM > 0 ? frag_lds_bytes<(TBM > 0 ? TBM : BM), FN, S, 4>() : 0;
+  constexpr size_t lds = lds_full > lds_tail ? lds_full : lds_tail;
   static bool attr_set = false;
   if (!attr_set) {
-    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_fp8_kernel<BM, FN, S, WPE, SPLIT>),
+    DN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_fp8_kernel<BM, FN, S, WPE, SPLIT, TBM>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
     attr_set = true;
   }
   const int mt = ceil_div(p.M, BM), nt = ceil_div(p.N, 32 * FN * 4);
-  hipLaunchKernelGGL((gemm_fp8_kernel<BM, FN, S, WPE, SPLIT>), dim3(mt * nt * nsplit), dim3(256), lds, s, p, mt, nt,
-                     nsplit);
+  int grid = mt * nt * nsplit, tail_full = 0;
+  if (TBM > 0 && tail_bands > 0) {
+    tail_full = mt * (nt - tail_bands);
+    const int tail = ceil_div(p.M, TBM > 0 ? TBM : BM) * tail_bands;
+    DN_CHECK(nsplit == 1 && tail_bands < nt && tail_full % kXcds == 0 && tail % kXcds == 0,
+             "gemm_fp8: tail tiles need no split and tile counts divisible by the XCD count");
+    grid = tail_full + tail;
+  }
+  hipLaunchKernelGGL((gemm_fp8_kernel<BM, FN, S, WPE, SPLIT, TBM>), dim3(grid), dim3(256), lds, s, p, mt, nt, nsplit,
+                     tail_full, TBM > 0 ? tail_bands : 0);
   DN_HIP(hipGetLastError());
 }
 
@@ -1231,11 +1264,13 @@ GemmPlan gemm_plan_fp8(int M, int N, int K, int geglu, int cus, bool allow_split
     g.bm = 128;
     g.bn = (geglu || N >= 1024) ? 256 : 128;
     g.split = 1;
+    g.tail_bands = 0;
   }
   while (g.split > 1 && K / 128 < 2 * g.split) --g.split;
   g.frag = 1;
   g.stages = 3;
-  g.tail_bands = 0;
+  // the bf16 planner's tail bands hold for the same 128 x 256 grid (two workgroups per CU)
+  if (!(g.bn == 256 && g.split == 1)) g.tail_bands = 0;
   return g;
 }
 
@@ -1252,7 +1287,9 @@ void gemm_fp8(const GemmParams& p, const GemmPlan& g, hipStream_t s) {
     DN_CHECK(p.n_store % 4 == 0 && p.n_store == p.N, "gemm_fp8: split-K needs n_store == N, a multiple of 4");
     DN_CHECK(p.part && p.part_floats >= (size_t)g.split * p.M * p.n_store, "gemm_fp8: split-K workspace too small");
   }
-  if (g.bn == 256)
+  if (g.bn == 256 && g.split == 1 && g.tail_bands > 0 && !p.raw_partial)
+    launch_fp8<128, 2, 3, 2, false, 64>(p, 1, s, g.tail_bands);
+  else if (g.bn == 256)
     run_fp8<128, 2, 3, 2>(p, g.split, s);
   else
     run_fp8<128, 1, 3, 2>(p, g.split, s);
