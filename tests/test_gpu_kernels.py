@@ -36,7 +36,7 @@ def _rng(seed):
 @pytest.mark.parametrize("M,N,K", [(300, 200, 128), (512, 384, 640), (1000, 1280, 64), (64, 64, 1280),
                                    (2048, 2048, 128), (8192, 512, 256), (300, 1280, 2560), (77, 96, 1920),
                                    (1000, 640, 5120), (129, 256, 704), (2000, 1248, 1280), (8000, 608, 2560),
-                                   (8192, 200, 256), (16384, 640, 1280), (2048, 10240, 1280)])
+                                   (8192, 200, 256), (16384, 640, 1280), (2048, 10240, 1280), (16300, 608, 1280)])
 def test_linear(dtype, M, N, K):
     """Shapes cover every tile plan: in fp32 the register-staged 64 x 64 / 128 x 128
     tiles; in bf16 the row-major kernels for N % 32 != 0 (N = 200) and the fragment-B
@@ -45,7 +45,8 @@ def test_linear(dtype, M, N, K):
     tiles (2000 x 1248 x 1280, 8000 x 608 x 2560: one tile per CU, ragged last row tile
     and column tile), ragged M and N tails; a tall row-major case (8192 x 200 x 256); the
     four-wave 128 x 160 tiles, two per CU, that linear layers with more 160-column tiles
-    than CUs take (16384 x 640 x 1280, 2048 x 10240 x 1280). Outputs: bf16 / fp32 without residual, fp32
+    than CUs take (16384 x 640 x 1280, 2048 x 10240 x 1280; 16300 x 608 x 1280 with a ragged
+    last row tile and column tile). Outputs: bf16 / fp32 without residual, fp32
     with an fp32 residual, and the op's dtype with a residual in that dtype."""
     announce(f"linear dtype={dtype} M={M} N={N} K={K}")
     r = _rng(M + N + K)
@@ -78,10 +79,11 @@ def _interleave(w1, n):
 
 
 @pytest.mark.parametrize("dtype", DT)
-@pytest.mark.parametrize("M,N,K", [(300, 96, 128), (512, 1280, 320), (2048, 5120, 1280)])
+@pytest.mark.parametrize("M,N,K", [(300, 96, 128), (512, 1280, 320), (2048, 5120, 1280), (2000, 5120, 1280)])
 def test_linear_geglu(dtype, M, N, K):
     """Ragged small shapes and SD-XL's FF-in at full size, whole output: in bf16 its 640
-    128 x 256 tiles leave a quarter round, whose column bands run as 64-row tiles."""
+    128 x 256 tiles leave a quarter round, whose column bands run as 64-row tiles (with a
+    ragged last row tile of both kinds at 2000 rows)."""
     announce(f"geglu dtype={dtype} M={M} N={N} K={K}")
     r = _rng(7 * M + N)
     x, xh = to_dev(r.standard_normal((M, K)), dtype)
@@ -101,13 +103,14 @@ def test_linear_geglu(dtype, M, N, K):
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("n,H,W,Cin,Cout,up,stride", [
     (2, 9, 7, 64, 96, 0, 1), (2, 9, 7, 64, 96, 0, 2), (1, 5, 6, 128, 64, 1, 1), (2, 16, 16, 128, 320, 0, 1),
-    (2, 128, 128, 320, 320, 0, 1), (2, 128, 128, 640, 320, 0, 1), (1, 64, 64, 640, 640, 1, 1)])
+    (2, 128, 128, 320, 320, 0, 1), (2, 128, 128, 640, 320, 0, 1), (1, 64, 64, 640, 640, 1, 1),
+    (2, 100, 100, 320, 320, 0, 1)])
 def test_conv3x3(dtype, n, H, W, Cin, Cout, up, stride):
     """Small shapes with ragged tiles, and the SD-XL convolutions at full size, whole
     output against the oracle: the 128x128-level ResBlock convolutions (32768 rows, 320
     channels from 320 and from a 640-channel input) and the nearest-x2 upsampling
     convolution into that level (640 channels): in bf16 these run on the four-wave
-    160-column tiles, two workgroups per CU."""
+    160-column tiles, two workgroups per CU; 2 x 100 x 100 has a ragged last row tile."""
     announce(f"conv dtype={dtype} n={n} H={H} W={W} Cin={Cin} Cout={Cout} up={up} stride={stride}")
     r = _rng(n * H * W + Cin + Cout + up + stride)
     x, xh = to_dev(r.standard_normal((n, H, W, Cin)), dtype)
@@ -430,7 +433,7 @@ def test_fp8_pack_matches_oracle_quantization(N, K):
 
 @pytest.mark.parametrize("M,N,K,geglu,resid", [(300, 256, 256, False, False), (2048, 1280, 5120, False, True),
                                                (1000, 640, 1280, False, True), (300, 256, 128, True, False),
-                                               (2048, 5120, 1280, True, False)])
+                                               (2048, 5120, 1280, True, False), (2000, 5120, 1280, True, False)])
 def test_fp8_linear(M, N, K, geglu, resid):
     """The fp8 GEMM against the oracle on the quantised operands: fp32 output within
     1e-5 (products exact, fp32 sums in another order); the GEGLU output in E4M3 against
