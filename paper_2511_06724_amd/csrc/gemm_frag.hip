@@ -5,8 +5,11 @@
 //  - B, the packed weight matrix, is stored in MFMA fragment order (to_frag, below):
 //    for each block of 32 output columns and each k-step of 16, the 64 lanes' 16-byte
 //    operands lie in 1 KB of contiguous memory. Each wave loads its own B fragments
-//    with one coalesced 16-byte load per lane straight into registers, one or two LDS
-//    stages ahead, so B costs no LDS bandwidth;
+//    with one coalesced 16-byte load per lane straight into registers, one to three LDS
+//    stages ahead, so B costs no LDS bandwidth (as far ahead as the A stages where the
+//    registers allow: the compiler, which does not see the A loads, waits for a B
+//    register by counting B loads only, so each such wait also retires the oldest A
+//    loads issued after that B load);
 //  - A (the activations, or the implicit-convolution gather) goes global -> LDS with
 //    global_load_lds_dwordx4 into S stages of BK = 64 (128-byte rows, chunk c of row r
 //    at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1)), shared by the waves (four
@@ -28,7 +31,10 @@
 //    columns keep the register layout, where consecutive lanes are consecutive tokens.
 //  - tiles go to XCDs in contiguous ranges (workgroup ids are dealt round-robin over the
 //    8 XCDs), ordered by column band, split, then row tile, so that the units sharing a
-//    band of B run on one XCD and share its L2.
+//    band of B run on one XCD and share its L2;
+//  - a 128 x 256 grid whose last round would be at most half full runs its last column
+//    bands as 64-row tiles in the same launch (a wrapper decodes full and tail units), so
+//    that the fraction of a round spreads over every CU.
 #include <algorithm>
 #include <type_traits>
 

@@ -58,7 +58,9 @@ struct GemmParams {
 // Block tile (bm x bn) of one GEMM launch and the kernel that runs it.
 struct GemmPlan {
   int bm, bn;
-  int stages = 2;        // fragment-B kernel: LDS pipeline depth
+  int stages = 2;        // fragment-B kernel variant: 3 the default (three LDS stages), 2 the 128 x 256
+                         // tile at one workgroup per CU, 5 the 160-column tile on four waves,
+                         // 13 / 14 stage read-ahead with three / four stages
   int frag = 0;          // 1: bf16 fragment-B kernel (gemm_frag.hip), else the register-staged kernel
   int split = 1;         // fragment-B kernel: K split in this many ranges (fp32 partials + reduce)
   int tail_bands = 0;    // fragment-B 128 x 256 tiles: the last column bands as 64-row tiles
