@@ -611,6 +611,14 @@ def main():
     roof = roofline_ff_in(torch, dn, stream)
     print(f"[bench] roofline FF-in {roof['avg_launch_us']} us (evicted), {roof['warm_avg_launch_us']} us (warm)",
           file=sys.stderr, flush=True)
+    sus_tf, sus_ghz = dn.probe_mfma_rate()
+    sustained = {"tflops": round(sus_tf, 1), "clock_ghz": round(sus_ghz, 3),
+                 "of_published_peak": round(sus_tf / PEAK_BF16_TFLOPS, 4),
+                 "ff_in_frac_of_sustained": round(roof["achieved"] / sus_tf, 4),
+                 "whole_step_frac_of_sustained": round(mfma_util * PEAK_BF16_TFLOPS / sus_tf, 4),
+                 "how": "dn_probe_mfma_rate: every CU, one wave per SIMD, back-to-back independent 32x32x16 "
+                        "bf16 MFMAs; event time of the launch, clock from the waves' cycle counts"}
+    print(f"[bench] matrix cores sustain {sus_tf:.0f} TFLOP/s at {sus_ghz:.2f} GHz", file=sys.stderr, flush=True)
     ac = None if args.no_ac else ac_sweep(torch, dn, model, cfg, ctx, ts, per_k=args.ac_queries)
     model.close()
     torch.cuda.empty_cache()
@@ -651,6 +659,7 @@ def main():
         "mfma_util_whole_step": round(mfma_util, 4),
         "output_finite": finite,
         "roofline": roof,
+        "mfma_sustained": sustained,
         "ac_sweep": ac,
         **extra,
         "cpu_baseline": cpu,

@@ -405,6 +405,15 @@ dn_status dn_op_layernorm_slabs(int32_t dtype, float* x, void* y, int64_t M, int
                                 const float* beta, float eps, const float* slabs, int32_t nsplit, const float* bias,
                                 int32_t resid, void* stream);
 
+/* Measurement entry point, not a step of the method: the bf16 rate the matrix cores of
+ * the current device sustain and the shader clock they hold meanwhile, the ceiling the
+ * GEMM and attention rooflines are read against beside the published peak. One
+ * workgroup of four waves per CU issues `iters` (1 .. 2^20) rounds of eight independent
+ * 32x32x16 bf16 MFMAs per wave; *tflops (host) = MFMA FLOPs / event time of the launch
+ * (after one untimed launch), *clock_ghz (host) = the waves' cycle counts over the 100 MHz
+ * constant counter. Synchronous (default stream); allocates and frees a few KB. */
+dn_status dn_probe_mfma_rate(int32_t iters, double* tflops, double* clock_ghz);
+
 /* ---------------------------------------------------------------------------
  * Latent decoder: the VAE Decoder of Table 3 (0.050 B parameters, 2481 GFLOP for a
  * 512 x 512 image), run once per image after the denoise loop to turn the final

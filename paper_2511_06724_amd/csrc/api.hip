@@ -18,6 +18,12 @@ constexpr size_t kScratchWinnerBytes = 256 * 1024;
 constexpr size_t kScratchBytes = kScratchWinnerBytes + 64 * sizeof(float);
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
+namespace dn {
+// probe.hip: the bf16 matrix-core rate (TFLOP/s) every CU sustains on back-to-back
+// 32x32x16 MFMAs and the shader clock (GHz) meanwhile. Synchronous.
+void mfma_rate(int iters, double* tflops, double* clock_ghz);
+}  // namespace dn
+
 namespace {
 
 constexpr int kMaxDevices = 64;
@@ -675,6 +681,14 @@ dn_status dn_op_layernorm_slabs(int32_t dtype, float* x, void* y, int64_t M, int
     else
       dn::layernorm_reduce<float>(x, static_cast<float*>(y), M, C, gamma, beta, eps, slabs, nsplit, bias,
                                   resid != 0, as_stream(stream));
+  });
+}
+
+dn_status dn_probe_mfma_rate(int32_t iters, double* tflops, double* clock_ghz) {
+  return guarded([&] {
+    DN_CHECK(tflops && clock_ghz, "dn_probe_mfma_rate: null pointer");
+    DN_CHECK(iters >= 1 && iters <= (1 << 20), "dn_probe_mfma_rate: iters must be in [1, 2^20]");
+    dn::mfma_rate(iters, tflops, clock_ghz);
   });
 }
 

@@ -24,6 +24,7 @@ MAX_LEVELS = 4
 EXPORTED = ("dn_weight_count", "dn_weight_table", "dn_create", "dn_denoise", "dn_denoise_capture", "dn_unet_eps", "ac_lookup",
             "ac_lookup_batch", "ac_lookup_batch_k", "ac_lookup_batch_noalloc", "ac_fetch_latent", "dn_packed_weight_elems", "dn_pack_weight", "dn_op_linear", "dn_op_conv3x3",
             "dn_op_attention", "dn_op_groupnorm", "dn_op_layernorm", "dn_op_layernorm_slabs", "dn_op_linear_vt",
+            "dn_probe_mfma_rate",
             "dn_destroy", "dn_last_error", "dn_vae_weight_count", "dn_vae_weight_table", "dn_vae_create",
             "dn_vae_decode", "dn_vae_destroy", "argus_oda", "argus_route", "argus_select_worker", "argus_last_error")
 
@@ -99,6 +100,7 @@ def _load():
         "dn_op_groupnorm": [I32, P, P, I32, I32, I32, I32, P, P, F32, I32, P],
         "dn_op_layernorm": [I32, P, P, I64, I32, P, P, F32, P],
         "dn_op_layernorm_slabs": [I32, P, P, I64, I32, P, P, F32, P, I32, P, I32, P],
+        "dn_probe_mfma_rate": [I32, C.POINTER(C.c_double), C.POINTER(C.c_double)],
         "argus_oda": [P, P, I32, P],
         "argus_route": [P, I32, I32, C.c_double, C.POINTER(I32)],
         "argus_select_worker": [P, P, P, I32, I32, C.POINTER(I32)],
@@ -411,6 +413,14 @@ def op_layernorm(dtype, x, y, M, Cc, gamma, beta, eps, stream=None):
 def op_layernorm_slabs(dtype, x, y, M, Cc, gamma, beta, eps, slabs, nsplit, bias=None, resid=True, stream=None):
     _check(lib.dn_op_layernorm_slabs(dtype, _ptr(x), _ptr(y), M, Cc, _ptr(gamma), _ptr(beta), eps, _ptr(slabs), nsplit,
                                      _ptr(bias), int(resid), _stream(stream)))
+
+
+def probe_mfma_rate(iters=4000):
+    """(TFLOP/s, GHz): the bf16 matrix-core rate the device sustains and its clock
+    meanwhile (dn_probe_mfma_rate; a measurement, not a step of the method)."""
+    tf, ghz = C.c_double(0.0), C.c_double(0.0)
+    _check(lib.dn_probe_mfma_rate(iters, C.byref(tf), C.byref(ghz)))
+    return tf.value, ghz.value
 
 
 # ----------------------------------------------------------------------------- routing control plane (host)

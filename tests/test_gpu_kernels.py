@@ -278,6 +278,21 @@ def test_layernorm_slabs(dtype, M, C, nsplit, bias, resid):
     assert rel_l2(host(y), ref) < (2e-6 if dtype == dn.DN_FP32 else TOL[dtype])
 
 
+def test_probe_mfma_rate():
+    """The matrix-core probe the bench reports beside the published peak: a rate and a
+    clock in the range the device can reach (at most the published 2.5 PFLOP/s at 2.4 GHz),
+    and an argument error for an iteration count out of range."""
+    announce("probe mfma rate")
+    tf, ghz = dn.probe_mfma_rate(2000)
+    assert 500.0 < tf <= 2600.0
+    assert 0.5 < ghz <= 2.6
+    # 32x32x16 MFMAs at one per 32 cycles per SIMD: the rate follows from the clock
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert tf <= cus * 4 * 32768 / 32 * ghz * 1e9 / 1e12 * 1.05
+    with pytest.raises(dn.DnError):
+        dn.probe_mfma_rate(0)
+
+
 def test_layernorm_slabs_argument_errors():
     x = torch.zeros((4, 64), device=DEV)
     y = torch.zeros((4, 64), device=DEV)
