@@ -22,6 +22,7 @@
  *   dn_unet_eps                        one UNet evaluation + guidance (per-step check hook)
  *   dn_vae_*                           the latent decoder after the loop (Table 3's VAE Decoder)
  *   dn_op_*                            single-kernel entry points (kernel checks, timing)
+ *   dn_probe_mfma_rate                 measurement: the matrix-core rate the device sustains
  *   dn_destroy, dn_last_error
  *   argus_oda, argus_route, argus_select_worker   routing control plane on the host (Sec. 4.3-4.4)
  *
@@ -60,7 +61,7 @@ typedef enum {
   DN_EINVAL = -1,       /* invalid argument or configuration */
   DN_ENOMEM = -2,       /* device or host allocation failed */
   DN_EHIP = -3,         /* HIP runtime error */
-  DN_EUNSUPPORTED = -4  /* valid but not supported by this build (e.g. no gfx950 device) */
+  DN_EUNSUPPORTED = -4  /* valid but not supported by the library as built (e.g. no gfx950 device) */
 } dn_status;
 
 typedef enum { DN_FP32 = 0, DN_BF16 = 1, DN_FP8 = 2 } dn_dtype;
