@@ -10,7 +10,9 @@
 //      in fp64 in a fixed order and writes per-(sample, channel) scale and shift
 //      (gamma * rstd, beta - mean * gamma * rstd);
 //   3. apply: y = x * scale + shift (then SiLU), one FMA per element, 16-byte
-//      vectors, a (pixel block, sample) grid.
+//      vectors, a (pixel block, sample) grid; up to 256 vectors per pixel a thread
+//      keeps one channel vector's scale and shift and walks pixels, beyond that the
+//      threads walk (pixel, vector) pairs.
 // The input may be the channel concatenation of two tensors (the up path's
 // [h, skip]); the output is always one contiguous tensor.
 //
@@ -233,6 +235,71 @@ __global__ __launch_bounds__(256) void gn_apply_kernel(GroupNormParams p, GnGeom
   }
 }
 
+// Apply with one channel vector per thread, for V <= 256 vectors per pixel: the 256
+// threads are 256 / V pixel lanes of V channel vectors; a thread loads the scale and shift
+// of its vector once, then its pixel lane's kApplyBatch pixels of the block, every load
+// issued before the first is used. Same arithmetic per element as gn_apply_kernel.
+constexpr int kApplyBatch = 8;
+
+template <typename T>
+__global__ __launch_bounds__(256) void gn_apply_cv_kernel(GroupNormParams p, GnGeom g, int pix_per_block) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int V = g.V;
+  const int lanes = 256 / V;
+  const int pl = threadIdx.x / V, r = threadIdx.x - (threadIdx.x / V) * V;
+  if (pl >= lanes) return;
+  const int n = blockIdx.y;
+  const int pix0 = blockIdx.x * pix_per_block;
+  const int npix = min(pix_per_block, p.HW - pix0);
+  const int c = r * VEC;
+  const float* scale = p.stats + (long long)n * g.C;
+  const float* shift = p.stats + (long long)(p.n + n) * g.C;
+  float4 sc[VEC / 4], sh[VEC / 4];
+#pragma unroll
+  for (int e = 0; e < VEC / 4; ++e) {
+    sc[e] = *reinterpret_cast<const float4*>(scale + c + 4 * e);
+    sh[e] = *reinterpret_cast<const float4*>(shift + c + 4 * e);
+  }
+  const bool first = c < p.c0;
+  const T* src = first ? static_cast<const T*>(p.x0) : static_cast<const T*>(p.x1);
+  const int ld = first ? p.c0 : p.c1;
+  const int cs = first ? c : c - p.c0;
+  const long long rowbase = (long long)n * p.HW + pix0;
+  for (int q0 = pl; q0 < npix; q0 += lanes * kApplyBatch) {
+    uint4 raw[kApplyBatch];
+#pragma unroll
+    for (int u = 0; u < kApplyBatch; ++u) {
+      const int q = min(q0 + u * lanes, npix - 1);
+      raw[u] = ld16(src + (rowbase + q) * ld + cs);
+    }
+#pragma unroll
+    for (int u = 0; u < kApplyBatch; ++u) {
+      const int q = q0 + u * lanes;
+      if (q >= npix) continue;
+      const T* xv = reinterpret_cast<const T*>(&raw[u]);
+      uint4 outv;
+      T* ov = reinterpret_cast<T*>(&outv);
+#pragma unroll
+      for (int e = 0; e < VEC; e += 4) {
+        const float4 a = sc[e / 4], bsh = sh[e / 4];
+        float v0 = to_f32(xv[e + 0]) * a.x + bsh.x, v1 = to_f32(xv[e + 1]) * a.y + bsh.y;
+        float v2 = to_f32(xv[e + 2]) * a.z + bsh.z, v3 = to_f32(xv[e + 3]) * a.w + bsh.w;
+        if (p.silu) {
+          v0 = silu_f(v0);
+          v1 = silu_f(v1);
+          v2 = silu_f(v2);
+          v3 = silu_f(v3);
+        }
+        ov[e + 0] = from_f32<T>(v0);
+        ov[e + 1] = from_f32<T>(v1);
+        ov[e + 2] = from_f32<T>(v2);
+        ov[e + 3] = from_f32<T>(v3);
+      }
+      st16(static_cast<T*>(p.y) + (rowbase + q) * g.C + c, outv);
+    }
+  }
+}
+
 constexpr int kLnMaxVec = 8;  // float4 vectors per lane: C <= 2048
 
 template <typename T> struct Store4;
@@ -387,8 +454,13 @@ template <typename T> void groupnorm(const GroupNormParams& p, hipStream_t s) {
   const GnGeom g = gn_geom<T>(p.HW, C);
   hipLaunchKernelGGL(gn_partial_kernel<T>, dim3(g.chunks, p.n, g.vslices), dim3(256), 0, s, p, g);
   hipLaunchKernelGGL(gn_finalize_kernel, dim3(p.G, p.n), dim3(256), 0, s, p, g);
-  const int ppb = (kApplyVecs + g.V - 1) / g.V;
-  hipLaunchKernelGGL(gn_apply_kernel<T>, dim3((p.HW + ppb - 1) / ppb, p.n), dim3(256), 0, s, p, g, ppb);
+  if (g.V <= 256) {
+    const int ppb = (256 / g.V) * kApplyBatch;
+    hipLaunchKernelGGL(gn_apply_cv_kernel<T>, dim3((p.HW + ppb - 1) / ppb, p.n), dim3(256), 0, s, p, g, ppb);
+  } else {
+    const int ppb = (kApplyVecs + g.V - 1) / g.V;
+    hipLaunchKernelGGL(gn_apply_kernel<T>, dim3((p.HW + ppb - 1) / ppb, p.n), dim3(256), 0, s, p, g, ppb);
+  }
   DN_HIP(hipGetLastError());
 }
 
