@@ -7,7 +7,8 @@
 //      never mix channels; per-channel sums meet in LDS, then one thread per group adds
 //      the group's channels in that slice, zero for groups outside it);
 //   2. finalize: one workgroup per (sample, group) merges the (chunk, slice) partials
-//      in fp64 in a fixed order and writes per-(sample, channel) scale and shift
+//      in fp64 in a fixed order (per thread, over the wave, over the four waves) and
+//      writes per-(sample, channel) scale and shift
 //      (gamma * rstd, beta - mean * gamma * rstd);
 //   3. apply: y = x * scale + shift (then SiLU), one FMA per element, 16-byte
 //      vectors, a (pixel block, sample) grid; up to 256 vectors per pixel a thread
@@ -130,8 +131,8 @@ __global__ __launch_bounds__(256) void gn_partial_kernel(GroupNormParams p, GnGe
 }
 
 __global__ __launch_bounds__(256) void gn_finalize_kernel(GroupNormParams p, GnGeom g) {
-  __shared__ double rs[256], rq[256];
-  const int tid = threadIdx.x;
+  __shared__ double ws[4], wq[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = blockIdx.x, n = blockIdx.y;
   const int cg = g.C / p.G;
   const int items = g.chunks * g.vslices;
@@ -141,19 +142,23 @@ __global__ __launch_bounds__(256) void gn_finalize_kernel(GroupNormParams p, GnG
     s += in[0];
     q += in[1];
   }
-  rs[tid] = s;
-  rq[tid] = q;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (tid < w) {
-      rs[tid] += rs[tid + w];
-      rq[tid] += rq[tid + w];
-    }
-    __syncthreads();
+  // a butterfly over the wave (lane 0's order of additions is fixed), then the four
+  // waves in order
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    s += __shfl_xor(s, o, 64);
+    q += __shfl_xor(q, o, 64);
   }
+  if (lane == 0) {
+    ws[wave] = s;
+    wq[wave] = q;
+  }
+  __syncthreads();
+  const double S = (ws[0] + ws[1]) + (ws[2] + ws[3]);
+  const double Q = (wq[0] + wq[1]) + (wq[2] + wq[3]);
   const double cnt = (double)cg * p.HW;
-  const double mean = rs[0] / cnt;
-  const double var = fmax(rq[0] / cnt - mean * mean, 0.0);
+  const double mean = S / cnt;
+  const double var = fmax(Q / cnt - mean * mean, 0.0);
   const double rstd = 1.0 / sqrt(var + (double)p.eps);
   for (int j = tid; j < cg; j += 256) {
     const int c = grp * cg + j;
