@@ -214,10 +214,13 @@ def test_linear_vt(dtype, M, seq, heads, dp, K):
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("n,HW,C,G,silu", [(2, 300, 320, 32, 1), (2, 64, 64, 32, 0), (1, 1000, 1920, 32, 1),
                                             (2, 1024, 1280, 32, 1), (2, 4096, 640, 32, 0), (1, 16384, 320, 32, 1),
-                                            (2, 200, 96, 32, 1)])
+                                            (2, 200, 96, 32, 1), (2, 1024, 2560, 32, 1)])
 def test_groupnorm(dtype, n, HW, C, G, silu):
     """Includes the SD-XL shapes (40, 20 and 10 channels per group at 32x32, 64x64 and
-    128x128) and an odd channel count per group (96 / 32 = 3)."""
+    128x128, and the 2560-channel concatenation at 32x32), an odd channel count per group
+    (96 / 32 = 3), and both apply mappings: one channel vector per thread (at most 256
+    16-byte vectors per pixel) and (pixel, vector) pairs (fp32 from 1280 channels, bf16 at
+    2560)."""
     announce(f"groupnorm dtype={dtype} n={n} HW={HW} C={C} silu={silu}")
     r = _rng(n + HW + C)
     x, xh = to_dev(0.5 + 2.0 * r.standard_normal((n, HW, C)), dtype)
